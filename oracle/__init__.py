@@ -1,0 +1,243 @@
+"""CPU oracle for MXNorm and RMSNorm + MX cast -- TEST INFRASTRUCTURE ONLY.
+
+Only the test suite, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  The product path (the HIP library and
+its Python binding) never imports, links or calls it, and the two share no
+code.  The arithmetic lives in ``mx_oracle.c`` (plain C, one obviously-correct
+step at a time, citing the paper's sections, equations and algorithms); this
+module only builds that file with gcc and marshals numpy arrays to it.
+
+Paper: "MXNorm: Reusing MXFP block scales for efficient tensor normalisation",
+arXiv 2603.13180.  Algorithm 1 (RMSNorm + MXCast), Algorithm 2 (MXNorm),
+Sec. 3.1-3.4, and the implementation appendix's mx_norm / mx_quantise.
+"""
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "mx_oracle.c")
+_LIB = os.path.join(_HERE, "libmx_oracle.so")
+
+SCALE_MODES = {"rceil": 0, "floor": 1}
+MAX_D = 65536
+
+_lib = None
+
+
+def build(force=True):
+    """Compile mx_oracle.c with gcc (IEEE arithmetic: no FMA contraction, no
+    fast-math) into libmx_oracle.so next to it."""
+    if not force and os.path.exists(_LIB):
+        return _LIB
+    tmp = _LIB + ".tmp%d" % os.getpid()
+    cmd = ["gcc", "-O2", "-fPIC", "-shared", "-std=c99", "-ffp-contract=off",
+           "-fno-fast-math", "-Wall", "-Wextra", "-o", tmp, _SRC, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        build()
+    lib = ctypes.CDLL(_LIB)
+    P = ctypes.c_void_p
+    I64 = ctypes.c_int64
+    F = ctypes.c_float
+    I = ctypes.c_int
+    sig = {
+        "mxo_e4m3_value": (ctypes.c_double, [ctypes.c_uint8]),
+        "mxo_e2m1_value": (ctypes.c_double, [ctypes.c_uint8]),
+        "mxo_e8m0_value": (ctypes.c_double, [ctypes.c_uint8]),
+        "mxo_e4m3_encode": (ctypes.c_uint8, [F]),
+        "mxo_e2m1_encode": (ctypes.c_uint8, [F]),
+        "mxo_scale_exponent": (I, [F, I]),
+        "mxo_coef": (F, [I, I]),
+        "mxo_rms_inverse": (ctypes.c_double, [P, I64, F]),
+        "mxo_rho_from_absmax": (ctypes.c_double, [P, I64, I, F, F]),
+        "mxo_mxcast_mxfp8": (None, [P, I64, I64, I, P, P]),
+        "mxo_mxnorm_mxfp8": (None, [P, I64, I64, I, F, F, I, P, P, P, P]),
+        "mxo_rmsnorm_mxfp8": (None, [P, P, I64, I64, F, I, P, P, P, P]),
+        "mxo_mxnorm_nvfp4": (None, [P, I64, I64, I, F, F, F, P, P, P, P]),
+        "mxo_rmsnorm_nvfp4": (None, [P, P, I64, I64, F, F, P, P, P, P]),
+        "mxo_mxnorm_default_global_scale": (ctypes.c_double, [I64, I, I, F]),
+        "mxo_rmsnorm_default_global_scale": (ctypes.c_double, [I64, F]),
+        "mxo_e4m3_encode_array": (None, [P, I64, P]),
+        "mxo_e2m1_encode_array": (None, [P, I64, P]),
+        "mxo_scale_exponent_array": (None, [P, I64, I, P]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _as_bf16_rows(x):
+    x = np.ascontiguousarray(x)
+    if x.dtype != np.uint16 or x.ndim != 2:
+        raise TypeError("x must be a 2-D uint16 array of bf16 bit patterns")
+    if x.shape[1] > MAX_D:
+        raise ValueError("the oracle handles d <= %d" % MAX_D)
+    return x
+
+
+def _as_gamma(gamma, d):
+    if gamma is None:
+        return None
+    g = np.ascontiguousarray(gamma)
+    if g.dtype != np.uint16 or g.shape != (d,):
+        raise TypeError("gamma must be a uint16 array of %d bf16 bit patterns" % d)
+    return g
+
+
+# ----------------------------------------------------------------- formats --
+
+def e4m3_value(codes):
+    lib = _load()
+    return np.array([lib.mxo_e4m3_value(int(c)) for c in np.ravel(codes)]).reshape(np.shape(codes))
+
+
+def e2m1_value(codes):
+    lib = _load()
+    return np.array([lib.mxo_e2m1_value(int(c)) for c in np.ravel(codes)]).reshape(np.shape(codes))
+
+
+def e8m0_value(bytes_):
+    lib = _load()
+    return np.array([lib.mxo_e8m0_value(int(c)) for c in np.ravel(bytes_)]).reshape(np.shape(bytes_))
+
+
+def e4m3_encode(v):
+    v = np.ascontiguousarray(v, dtype=np.float32)
+    out = np.empty(v.shape, np.uint8)
+    _load().mxo_e4m3_encode_array(_ptr(v), v.size, _ptr(out))
+    return out
+
+
+def e2m1_encode(v):
+    v = np.ascontiguousarray(v, dtype=np.float32)
+    out = np.empty(v.shape, np.uint8)
+    _load().mxo_e2m1_encode_array(_ptr(v), v.size, _ptr(out))
+    return out
+
+
+def scale_exponent(a, mode="rceil"):
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    out = np.empty(a.shape, np.int32)
+    _load().mxo_scale_exponent_array(_ptr(a), a.size, SCALE_MODES[mode], _ptr(out))
+    return out
+
+
+def coef(B, p):
+    """absmax_scale_factor(B, p) as a float32 constant."""
+    return float(_load().mxo_coef(B, p))
+
+
+def rms_inverse(x_f32, eps=0.0):
+    x = np.ascontiguousarray(x_f32, dtype=np.float32)
+    return float(_load().mxo_rms_inverse(_ptr(x), x.size, eps))
+
+
+def rho_from_absmax(m_f32, p=2, coef_=None, eps=0.0, B=32):
+    m = np.ascontiguousarray(m_f32, dtype=np.float32)
+    c = coef(B, p) if coef_ is None else coef_
+    return float(_load().mxo_rho_from_absmax(_ptr(m), m.size, p, c, eps))
+
+
+def mxnorm_default_global_scale(d, B=16, p=2, coef_=None):
+    c = coef(B, p) if coef_ is None else coef_
+    return float(_load().mxo_mxnorm_default_global_scale(d, B, p, c))
+
+
+def rmsnorm_default_global_scale(d, gamma_absmax=1.0):
+    return float(_load().mxo_rmsnorm_default_global_scale(d, gamma_absmax))
+
+
+# ------------------------------------------------------------------ casts --
+
+def mxcast_mxfp8(y, mode="rceil"):
+    """Plain MXFP8 cast (eq. blockscale / blockvals) of float32 y [T, d]."""
+    y = np.ascontiguousarray(y, dtype=np.float32)
+    T, d = y.shape
+    if d % 32:
+        raise ValueError("d must be a multiple of 32")
+    codes = np.empty((T, d), np.uint8)
+    scales = np.empty((T, d // 32), np.uint8)
+    _load().mxo_mxcast_mxfp8(_ptr(y), T, d, SCALE_MODES[mode], _ptr(codes), _ptr(scales))
+    return codes, scales
+
+
+def mxnorm_mxfp8(x, p=2, coef_=None, eps=1e-6, mode="rceil"):
+    """Algorithm 2 (MXNorm), E4M3 codes + E8M0 scales per 32-element block.
+    Returns (codes [T,d] u8, scales [T,d/32] u8, rho32 [T] f32, rho64 [T] f64)."""
+    x = _as_bf16_rows(x)
+    T, d = x.shape
+    if d % 32:
+        raise ValueError("d must be a multiple of 32")
+    c = coef(32, p) if coef_ is None else coef_
+    codes = np.empty((T, d), np.uint8)
+    scales = np.empty((T, d // 32), np.uint8)
+    r32 = np.empty(T, np.float32)
+    r64 = np.empty(T, np.float64)
+    _load().mxo_mxnorm_mxfp8(_ptr(x), T, d, p, c, eps, SCALE_MODES[mode], _ptr(codes),
+                             _ptr(scales), _ptr(r32), _ptr(r64))
+    return codes, scales, r32, r64
+
+
+def rmsnorm_mxfp8(x, gamma=None, eps=1e-6, mode="rceil"):
+    """Algorithm 1 (RMSNorm, optional gain, then MXCast)."""
+    x = _as_bf16_rows(x)
+    T, d = x.shape
+    if d % 32:
+        raise ValueError("d must be a multiple of 32")
+    g = _as_gamma(gamma, d)
+    codes = np.empty((T, d), np.uint8)
+    scales = np.empty((T, d // 32), np.uint8)
+    r32 = np.empty(T, np.float32)
+    r64 = np.empty(T, np.float64)
+    _load().mxo_rmsnorm_mxfp8(_ptr(x), _ptr(g), T, d, eps, SCALE_MODES[mode], _ptr(codes),
+                              _ptr(scales), _ptr(r32), _ptr(r64))
+    return codes, scales, r32, r64
+
+
+def mxnorm_nvfp4(x, s_g, p=2, coef_=None, eps=1e-6):
+    """MXNorm with NVFP4 output: packed E2M1 codes [T, d/2], E4M3 scales [T, d/16]."""
+    x = _as_bf16_rows(x)
+    T, d = x.shape
+    if d % 16:
+        raise ValueError("d must be a multiple of 16")
+    c = coef(16, p) if coef_ is None else coef_
+    codes = np.empty((T, d // 2), np.uint8)
+    scales = np.empty((T, d // 16), np.uint8)
+    r32 = np.empty(T, np.float32)
+    r64 = np.empty(T, np.float64)
+    _load().mxo_mxnorm_nvfp4(_ptr(x), T, d, p, c, eps, s_g, _ptr(codes), _ptr(scales),
+                             _ptr(r32), _ptr(r64))
+    return codes, scales, r32, r64
+
+
+def rmsnorm_nvfp4(x, s_g, gamma=None, eps=1e-6):
+    x = _as_bf16_rows(x)
+    T, d = x.shape
+    if d % 16:
+        raise ValueError("d must be a multiple of 16")
+    g = _as_gamma(gamma, d)
+    codes = np.empty((T, d // 2), np.uint8)
+    scales = np.empty((T, d // 16), np.uint8)
+    r32 = np.empty(T, np.float32)
+    r64 = np.empty(T, np.float64)
+    _load().mxo_rmsnorm_nvfp4(_ptr(x), _ptr(g), T, d, eps, s_g, _ptr(codes), _ptr(scales),
+                              _ptr(r32), _ptr(r64))
+    return codes, scales, r32, r64

@@ -1,0 +1,537 @@
+/*
+ * mx_oracle.c -- plain, slow, obviously-correct CPU oracle for MXNorm and for
+ * RMSNorm followed by an MX cast.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path links, loads or calls
+ * this file: only the test suite, the smoke check and the benchmark's CPU
+ * baseline leg use it.  It shares no code, header, table or helper with the
+ * HIP kernels; it was written from the paper's definitions, one step at a
+ * time, in the paper's order:
+ *
+ *   "MXNorm: Reusing MXFP block scales for efficient tensor normalisation"
+ *   (McLean, Prince, Payot, Balanca, Luschi; arXiv 2603.13180)
+ *
+ *   - Sec. 3.1, eq. (rms) and eq. (gain): RMSNorm.
+ *   - Sec. 3.2, eq. (blockscale) and eq. (blockvals): the MX cast; RCEIL
+ *     power-of-two rounding (the rule the experiments used, Sec. 3.2).
+ *   - Algorithm 1 (RMSNorm + MXCast) and Algorithm 2 (MXNorm), with the
+ *     MXNorm equations of Sec. 3.4.
+ *   - Theorem 1 (Sec. 3.3) and the coefficient table absmax_scale_factor of
+ *     the appendix "Implementation of MXNormLinear".
+ *
+ * Readings where the paper is silent or garbled (each one is listed with its
+ * reason in the design notes of the repository):
+ *   R1  coef is the absmax_scale_factor table value (about 1/c of Theorem 1);
+ *       the RMS estimate is r = coef * G_p, and rho~ = 1/r (Sec. 3.4 and the
+ *       mx_norm function of the implementation appendix).
+ *   R2  the block absmax uses |X| (Alg. 2; the Sec. 3.4 equation drops the
+ *       bars).
+ *   R3  epsilon is added inside the square root, as RMSNorm does:
+ *       rho~ = (r^2 + eps)^(-1/2), rho = (mean x^2 + eps)^(-1/2).  When the
+ *       radicand is exactly zero, rho := 0 (the row is all zeros).
+ *   R4  E8M0 scale rule: RCEIL -- the smallest integer e with
+ *       a <= 448 * 2^e -- or FLOOR: e = floor(log2 a) - 8 (the literal
+ *       "divide by 256, round down" reading).  e is clamped to [-127, 127];
+ *       byte = e + 127; a non-finite a gives the NaN byte 0xFF.
+ *   R5  element casts round to nearest, ties to the even code, and saturate
+ *       to the largest finite magnitude (448 for E4M3, 6 for E2M1); the sign
+ *       bit is kept, also for zero results.
+ *   R6  element order of operations: t = RN32(x * rho~), v = t * 2^-e
+ *       (exact scaling), code = cast(v).  The block scale is decided from
+ *       a = RN32(m~ * rho~), which equals max_b |t| by monotonicity.
+ *   R7  precision: rho and rho~ are computed in double from a sequential
+ *       double sum and rounded once to float; everything that decides a code
+ *       is then done in IEEE single precision, the precision of the kernels.
+ *   R8  a block whose scale is NaN (non-finite input) has every code set to
+ *       the input element's sign bit with an all-ones magnitude (0x7F for
+ *       E4M3, 0x7 for E2M1).
+ *   R9  NVFP4 (16-element blocks, E4M3 block scale, fp32 tensor decode scale
+ *       s_g, E2M1 codes two per byte, even element in the low nibble):
+ *       q = a / RN32(6 s_g); S = E4M3(q); den = RN32(dec(S) s_g);
+ *       v = RN32(t / den); code = E2M1(v); if dec(S) == 0 every code of the
+ *       block is a signed zero.
+ *
+ * Build: gcc -O2 -fPIC -shared -ffp-contract=off -fno-fast-math -o ... -lm
+ * (no FMA contraction, no flush-to-zero; x86-64 SSE arithmetic is IEEE
+ * binary32/binary64 with round-to-nearest-even).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#define MXO_SCALE_RCEIL 0
+#define MXO_SCALE_FLOOR 1
+
+/* ------------------------------------------------------------------------ */
+/* Number formats                                                            */
+/* ------------------------------------------------------------------------ */
+
+/* bf16 is the upper half of an IEEE binary32: widening is exact. */
+float mxo_bf16_to_float(uint16_t b)
+{
+    uint32_t u = (uint32_t)b << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return f;
+}
+
+static int sign_of_bf16(uint16_t b) { return (b >> 15) & 1; }
+
+/* OCP E4M3 ("FN"): 1 sign, 4 exponent (bias 7), 3 mantissa bits; exponent
+ * field 0 is subnormal (m * 2^-9); S.1111.111 is NaN; no infinities.
+ * Largest finite magnitude 1.75 * 2^8 = 448. */
+double mxo_e4m3_value(uint8_t code)
+{
+    int s = (code >> 7) & 1, E = (code >> 3) & 0xF, M = code & 7;
+    double mag;
+    if (E == 15 && M == 7)
+        return NAN;
+    if (E == 0)
+        mag = ldexp((double)M, -9);
+    else
+        mag = ldexp(1.0 + M / 8.0, E - 7);
+    return s ? -mag : mag;
+}
+
+/* E2M1: 1 sign, 2 exponent (bias 1), 1 mantissa bit; values
+ * {0, 0.5, 1, 1.5, 2, 3, 4, 6}; no NaN, no infinity.  Uses the low nibble. */
+double mxo_e2m1_value(uint8_t code)
+{
+    int s = (code >> 3) & 1, E = (code >> 1) & 3, M = code & 1;
+    double mag = (E == 0) ? 0.5 * M : ldexp(1.0 + M / 2.0, E - 1);
+    return s ? -mag : mag;
+}
+
+/* E8M0: an unsigned biased exponent, value 2^(byte-127); 0xFF is NaN. */
+double mxo_e8m0_value(uint8_t byte)
+{
+    if (byte == 0xFF)
+        return NAN;
+    return ldexp(1.0, (int)byte - 127);
+}
+
+/* Round to the nearest representable value by exhaustive search over the
+ * non-negative finite codes; a tie picks the even code (the one whose
+ * mantissa LSB is zero), which is IEEE round-half-to-even.  Magnitudes at or
+ * above the largest finite value saturate to it (R5). */
+uint8_t mxo_e4m3_encode(float v)
+{
+    uint8_t s = signbit(v) ? 0x80 : 0x00;
+    double a, bestd = INFINITY;
+    int c, best = 0;
+    if (isnan(v))
+        return (uint8_t)(s | 0x7F);
+    a = fabs((double)v);
+    if (a >= 448.0)
+        return (uint8_t)(s | 0x7E);
+    for (c = 0; c <= 0x7E; c++) {
+        double dist = fabs(mxo_e4m3_value((uint8_t)c) - a);
+        if (dist < bestd || (dist == bestd && (c & 1) == 0)) {
+            bestd = dist;
+            best = c;
+        }
+    }
+    return (uint8_t)(s | best);
+}
+
+uint8_t mxo_e2m1_encode(float v)
+{
+    uint8_t s = signbit(v) ? 0x8 : 0x0;
+    double a, bestd = INFINITY;
+    int c, best = 0;
+    if (isnan(v))
+        return (uint8_t)(s | 0x7); /* R8: NaN only occurs in NaN blocks */
+    a = fabs((double)v);
+    if (a >= 6.0)
+        return (uint8_t)(s | 0x7);
+    for (c = 0; c <= 7; c++) {
+        double dist = fabs(mxo_e2m1_value((uint8_t)c) - a);
+        if (dist < bestd || (dist == bestd && (c & 1) == 0)) {
+            bestd = dist;
+            best = c;
+        }
+    }
+    return (uint8_t)(s | best);
+}
+
+/* E8M0 scale exponent for a block whose largest |value| is a (finite,
+ * non-negative), Sec. 3.2 eq. (blockscale) with the rounding rule R4.
+ * Returns e in [-127, 127]. */
+int mxo_scale_exponent(float a, int mode)
+{
+    int e;
+    if (mode == MXO_SCALE_RCEIL) {
+        /* smallest e with a <= 448 * 2^e: 448 * 2^e is exact in double */
+        e = -127;
+        while (e < 127 && (double)a > ldexp(448.0, e))
+            e++;
+        return e;
+    }
+    /* FLOOR: e = floor(log2 a) - 8, 256 = 2^8 being the largest power of two
+     * that E4M3 represents */
+    if (a == 0.0f)
+        return -127;
+    {
+        int E;
+        (void)frexp((double)a, &E); /* a = f * 2^E, f in [0.5, 1) */
+        e = (E - 1) - 8;
+    }
+    if (e < -127)
+        e = -127;
+    if (e > 127)
+        e = 127;
+    return e;
+}
+
+/* Scale byte of eq. (blockscale): NaN for a non-finite block maximum. */
+static uint8_t e8m0_byte_for(float a, int mode, int *e_out)
+{
+    if (!isfinite(a)) {
+        *e_out = 0;
+        return 0xFF;
+    }
+    *e_out = mxo_scale_exponent(a, mode);
+    return (uint8_t)(*e_out + 127);
+}
+
+/* absmax_scale_factor (appendix "Implementation of MXNormLinear"):
+ * Monte-Carlo estimates of RMS(X)/G_p for Gaussian X, as single-precision
+ * constants. */
+float mxo_coef(int B, int p)
+{
+    if (B == 16 && p == 1) return 0.4814f;
+    if (B == 16 && p == 2) return 0.4688f;
+    if (B == 32 && p == 1) return 0.4261f;
+    if (B == 32 && p == 2) return 0.4185f;
+    if (B == 64 && p == 1) return 0.3852f;
+    if (B == 64 && p == 2) return 0.3803f;
+    return NAN;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Row statistics                                                            */
+/* ------------------------------------------------------------------------ */
+
+/* m~_k = max_b |x_kb| (Alg. 2, first step; R2).  NaN propagates. */
+static float block_absmax(const float *x, int B)
+{
+    float m = 0.0f;
+    int b;
+    for (b = 0; b < B; b++) {
+        float ax = fabsf(x[b]);
+        if (isnan(ax))
+            return ax;
+        if (ax > m)
+            m = ax;
+    }
+    return m;
+}
+
+/* rho = (1/D sum_d x_d^2 + eps)^(-1/2)  (Sec. 3.1 eq. (rms); R3, R7) */
+double mxo_rms_inverse(const float *x, int64_t d, float eps)
+{
+    double s = 0.0, u;
+    int64_t i;
+    for (i = 0; i < d; i++)
+        s += (double)x[i] * (double)x[i];
+    u = s / (double)d + (double)eps;
+    if (u == 0.0)
+        return 0.0;
+    return 1.0 / sqrt(u);
+}
+
+/* rho~ from the block absmaxes (Alg. 2 second step, Sec. 3.4, and the
+ * implementation appendix's mx_norm):
+ * G_p = (1/K sum_k m~_k^p)^(1/p);  r = coef * G_p;  rho~ = (r^2 + eps)^(-1/2)
+ * (R1, R3, R7). */
+double mxo_rho_from_absmax(const float *m, int64_t K, int p, float coef, float eps)
+{
+    double s = 0.0, G, r, u;
+    int64_t k;
+    for (k = 0; k < K; k++)
+        s += (p == 1) ? (double)m[k] : (double)m[k] * (double)m[k];
+    G = (p == 1) ? s / (double)K : sqrt(s / (double)K);
+    r = (double)coef * G;
+    u = r * r + (double)eps;
+    if (u == 0.0)
+        return 0.0;
+    return 1.0 / sqrt(u);
+}
+
+/* ------------------------------------------------------------------------ */
+/* MX casts                                                                  */
+/* ------------------------------------------------------------------------ */
+
+/* Plain MXFP8 cast of one block of already-normalised values y (eq.
+ * (blockscale), eq. (blockvals)): m = max|y|, S = 2^e, V = E4M3(y / S).
+ * sign_src (bf16 inputs) supplies the sign bits used for NaN blocks (R8);
+ * when it is NULL the sign of y is used. */
+static uint8_t mxfp8_cast_block(const float *y, const uint16_t *sign_src, int B, int mode,
+                                uint8_t *codes)
+{
+    float m = block_absmax(y, B);
+    int e, b;
+    uint8_t byte = e8m0_byte_for(m, mode, &e);
+    for (b = 0; b < B; b++) {
+        if (byte == 0xFF) {
+            int sb = sign_src ? sign_of_bf16(sign_src[b]) : (signbit(y[b]) ? 1 : 0);
+            codes[b] = (uint8_t)((sb << 7) | 0x7F);
+        } else {
+            /* exact power-of-two scaling; a result below the fp32 normal range
+             * is far below E4M3's smallest subnormal and encodes as +-0 */
+            float v = (float)ldexp((double)y[b], -e);
+            codes[b] = mxo_e4m3_encode(v);
+        }
+    }
+    return byte;
+}
+
+/* MXCast of a float matrix [T, d] with 32-element blocks (Sec. 3.2), no
+ * normalisation.  Used to check that MXNorm's cast stage reduces to the plain
+ * MX cast. */
+void mxo_mxcast_mxfp8(const float *y, int64_t T, int64_t d, int mode, uint8_t *codes,
+                      uint8_t *scales)
+{
+    const int B = 32;
+    int64_t t, k, K = d / B;
+    for (t = 0; t < T; t++)
+        for (k = 0; k < K; k++)
+            scales[t * K + k] = mxfp8_cast_block(y + t * d + k * B, NULL, B, mode,
+                                                 codes + t * d + k * B);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Algorithm 2: MXNorm, MXFP8 output                                         */
+/* ------------------------------------------------------------------------ */
+
+/* x: bf16 bits [T, d]; codes: E4M3 [T, d]; scales: E8M0 [T, d/32];
+ * rho32 / rho64: the inverse RMS estimate per row (either may be NULL). */
+void mxo_mxnorm_mxfp8(const uint16_t *x, int64_t T, int64_t d, int p, float coef, float eps,
+                      int mode, uint8_t *codes, uint8_t *scales, float *rho32, double *rho64)
+{
+    const int B = 32;
+    int64_t K = d / B, t, k;
+    float xf[32];
+    for (t = 0; t < T; t++) {
+        const uint16_t *xr = x + t * d;
+        double rho_d;
+        float rho_f;
+        float m[512 * 4]; /* K <= 2048 (d <= 65536) */
+        /* step 1: block absmaxes of the raw input */
+        for (k = 0; k < K; k++) {
+            int b;
+            for (b = 0; b < B; b++)
+                xf[b] = mxo_bf16_to_float(xr[k * B + b]);
+            m[k] = block_absmax(xf, B);
+        }
+        /* step 2: the inverse RMS estimate from the K absmaxes */
+        rho_d = mxo_rho_from_absmax(m, K, p, coef, eps);
+        rho_f = (float)rho_d;
+        if (rho64) rho64[t] = rho_d;
+        if (rho32) rho32[t] = rho_f;
+        /* steps 3-4: block scale from m~ * rho~, then the element cast */
+        for (k = 0; k < K; k++) {
+            float a = m[k] * rho_f; /* R6: RN32(m~ rho~) */
+            int e, b;
+            uint8_t byte = e8m0_byte_for(a, mode, &e);
+            scales[t * K + k] = byte;
+            for (b = 0; b < B; b++) {
+                uint16_t xb = xr[k * B + b];
+                uint8_t *c = codes + t * d + k * B + b;
+                if (byte == 0xFF) {
+                    *c = (uint8_t)((sign_of_bf16(xb) << 7) | 0x7F);
+                } else {
+                    float tv = mxo_bf16_to_float(xb) * rho_f; /* RN32(x rho~) */
+                    float v = (float)ldexp((double)tv, -e);  /* exact */
+                    *c = mxo_e4m3_encode(v);
+                }
+            }
+        }
+    }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Algorithm 1: RMSNorm (optionally with gain) then MXCast, MXFP8 output      */
+/* ------------------------------------------------------------------------ */
+
+/* y = RN32(RN32(x rho) gamma), gamma optional (Sec. 3.1 eq. (gain)); then the
+ * plain MXFP8 cast of eq. (blockscale), eq. (blockvals). */
+void mxo_rmsnorm_mxfp8(const uint16_t *x, const uint16_t *gamma, int64_t T, int64_t d,
+                       float eps, int mode, uint8_t *codes, uint8_t *scales, float *rho32,
+                       double *rho64)
+{
+    const int B = 32;
+    int64_t K = d / B, t, k, i;
+    for (t = 0; t < T; t++) {
+        const uint16_t *xr = x + t * d;
+        double rho_d;
+        float rho_f;
+        float xf[65536];
+        for (i = 0; i < d; i++)
+            xf[i] = mxo_bf16_to_float(xr[i]);
+        rho_d = mxo_rms_inverse(xf, d, eps);
+        rho_f = (float)rho_d;
+        if (rho64) rho64[t] = rho_d;
+        if (rho32) rho32[t] = rho_f;
+        for (i = 0; i < d; i++) {
+            float y = xf[i] * rho_f;
+            if (gamma)
+                y = y * mxo_bf16_to_float(gamma[i]);
+            xf[i] = y;
+        }
+        for (k = 0; k < K; k++)
+            scales[t * K + k] = mxfp8_cast_block(xf + k * B, xr + k * B, B, mode,
+                                                 codes + t * d + k * B);
+    }
+}
+
+/* ------------------------------------------------------------------------ */
+/* NVFP4 variants (R9)                                                       */
+/* ------------------------------------------------------------------------ */
+
+/* Cast one 16-element block of normalised values t, whose largest magnitude
+ * is a, to an E4M3 block scale and E2M1 codes (one code per byte here). */
+static uint8_t nvfp4_cast_block(const float *tv, const uint16_t *sign_src, float a,
+                                float s_g, uint8_t *codes)
+{
+    const int B = 16;
+    float six_sg = 6.0f * s_g;
+    float q;
+    uint8_t S;
+    int b;
+    if (!isfinite(a)) { /* R8: the E4M3 NaN byte 0x7F marks the block */
+        for (b = 0; b < B; b++)
+            codes[b] = (uint8_t)((sign_of_bf16(sign_src[b]) << 3) | 0x7);
+        return 0x7F;
+    }
+    q = a / six_sg;      /* RN32 */
+    S = mxo_e4m3_encode(q); /* q >= 0: satfinite at 448 */
+    {
+        float den = (float)mxo_e4m3_value(S) * s_g;
+        for (b = 0; b < B; b++) {
+            if (den == 0.0f)
+                codes[b] = signbit(tv[b]) ? 0x8 : 0x0;
+            else
+                codes[b] = mxo_e2m1_encode(tv[b] / den);
+        }
+    }
+    return S;
+}
+
+static void pack_nibbles(const uint8_t *codes, int64_t n, uint8_t *packed)
+{
+    int64_t j;
+    for (j = 0; j < n / 2; j++)
+        packed[j] = (uint8_t)((codes[2 * j] & 0xF) | ((codes[2 * j + 1] & 0xF) << 4));
+}
+
+/* codes: packed E2M1 [T, d/2]; scales: E4M3 [T, d/16]. */
+void mxo_mxnorm_nvfp4(const uint16_t *x, int64_t T, int64_t d, int p, float coef, float eps,
+                      float s_g, uint8_t *codes, uint8_t *scales, float *rho32, double *rho64)
+{
+    const int B = 16;
+    int64_t K = d / B, t, k;
+    for (t = 0; t < T; t++) {
+        const uint16_t *xr = x + t * d;
+        float m[4096];
+        float xf[16], tv[16];
+        uint8_t c[16];
+        uint8_t rowcodes[65536];
+        double rho_d;
+        float rho_f;
+        for (k = 0; k < K; k++) {
+            int b;
+            for (b = 0; b < B; b++)
+                xf[b] = mxo_bf16_to_float(xr[k * B + b]);
+            m[k] = block_absmax(xf, B);
+        }
+        rho_d = mxo_rho_from_absmax(m, K, p, coef, eps);
+        rho_f = (float)rho_d;
+        if (rho64) rho64[t] = rho_d;
+        if (rho32) rho32[t] = rho_f;
+        for (k = 0; k < K; k++) {
+            int b;
+            float a = m[k] * rho_f;
+            for (b = 0; b < B; b++)
+                tv[b] = mxo_bf16_to_float(xr[k * B + b]) * rho_f;
+            scales[t * K + k] = nvfp4_cast_block(tv, xr + k * B, a, s_g, c);
+            for (b = 0; b < B; b++)
+                rowcodes[k * B + b] = c[b];
+        }
+        pack_nibbles(rowcodes, d, codes + t * (d / 2));
+    }
+}
+
+void mxo_rmsnorm_nvfp4(const uint16_t *x, const uint16_t *gamma, int64_t T, int64_t d,
+                       float eps, float s_g, uint8_t *codes, uint8_t *scales, float *rho32,
+                       double *rho64)
+{
+    const int B = 16;
+    int64_t K = d / B, t, k, i;
+    for (t = 0; t < T; t++) {
+        const uint16_t *xr = x + t * d;
+        float xf[65536];
+        uint8_t rowcodes[65536];
+        double rho_d;
+        float rho_f;
+        for (i = 0; i < d; i++)
+            xf[i] = mxo_bf16_to_float(xr[i]);
+        rho_d = mxo_rms_inverse(xf, d, eps);
+        rho_f = (float)rho_d;
+        if (rho64) rho64[t] = rho_d;
+        if (rho32) rho32[t] = rho_f;
+        for (i = 0; i < d; i++) {
+            float y = xf[i] * rho_f;
+            if (gamma)
+                y = y * mxo_bf16_to_float(gamma[i]);
+            xf[i] = y;
+        }
+        for (k = 0; k < K; k++) {
+            float a = block_absmax(xf + k * B, B);
+            scales[t * K + k] = nvfp4_cast_block(xf + k * B, xr + k * B, a, s_g,
+                                                 rowcodes + k * B);
+        }
+        pack_nibbles(rowcodes, d, codes + t * (d / 2));
+    }
+}
+
+/* Default NVFP4 tensor decode scales: the output bound divided by the largest
+ * product of E2M1 and E4M3 magnitudes (6 * 448), so the bound maps onto the
+ * top of the representable range.  MXNorm uses Lemma 2's bound K^(1/p)/coef;
+ * RMSNorm uses Lemma 1's sqrt(d), times max|gamma|. */
+double mxo_mxnorm_default_global_scale(int64_t d, int B, int p, float coef)
+{
+    double K = (double)(d / B);
+    double bound = (p == 1 ? K : sqrt(K)) / (double)coef;
+    return bound / (6.0 * 448.0);
+}
+
+double mxo_rmsnorm_default_global_scale(int64_t d, float gamma_absmax)
+{
+    return sqrt((double)d) * (double)gamma_absmax / (6.0 * 448.0);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Array forms of the codec, for the tests' exhaustive sweeps                */
+/* ------------------------------------------------------------------------ */
+
+void mxo_e4m3_encode_array(const float *v, int64_t n, uint8_t *out)
+{
+    int64_t i;
+    for (i = 0; i < n; i++)
+        out[i] = mxo_e4m3_encode(v[i]);
+}
+
+void mxo_e2m1_encode_array(const float *v, int64_t n, uint8_t *out)
+{
+    int64_t i;
+    for (i = 0; i < n; i++)
+        out[i] = mxo_e2m1_encode(v[i]);
+}
+
+void mxo_scale_exponent_array(const float *a, int64_t n, int mode, int32_t *out)
+{
+    int64_t i;
+    for (i = 0; i < n; i++)
+        out[i] = mxo_scale_exponent(a[i], mode);
+}
