@@ -1,0 +1,237 @@
+"""Benchmark: MXNorm + MXFP8 cast throughput on one MI355X.
+
+A step is one forward pass of the fused MXNorm kernel (block absmax, row RMS
+estimate, E8M0 scales, E4M3 codes -- Algorithm 2) over the Llama-3-8B-shaped
+activation tensor x bf16 [32768, 4096] (seeded N(0,1) with 1% outlier
+channels).  The value is algorithmic HBM bytes per step (2 B read + 1 B code
++ 1/32 B scale per element, + 4 B of rho per row) divided by the measured
+step time.  Alongside, on the same inputs: the hand-written RMSNorm + MXFP8
+cast baseline (gain-free, as in the paper's kernel benchmark, and with gain),
+the NVFP4 variants, a device-to-device copy for reference, and the CPU oracle
+on a bounded sample.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
+Prints one JSON line.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBPS = 8000.0
+WORKLOAD = "llama3-8b-d4096"
+NV_WORKLOAD = "llama3-8b-d4096-nvfp4"
+ROTATE_MIN_BYTES = 768 << 20       # > 3x the 256 MiB Infinity Cache
+KERNEL_SRC = os.path.join(ROOT, "paper_2603_13180_amd", "csrc", "mxnorm.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_mxnorm_mxfp8_llama3-8b-d4096.txt")
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    return ap.parse_args()
+
+
+def mxfp8_bytes(T, d):
+    return T * d * 2 + T * d + T * (d // 32) + 4 * T
+
+
+def nvfp4_bytes(T, d):
+    return T * d * 2 + T * d // 2 + T * (d // 16) + 4 * T
+
+
+def source_hash():
+    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if
+    it was taken on the current kernel source; else None."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    kv = {}
+    for line in open(TRAFFIC_FILE):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("kernel_source_sha256_16") != source_hash():
+        return None
+    try:
+        return float(kv["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def time_launches(fn, n_sets, steps, warmup, stream):
+    import torch
+    for i in range(warmup):
+        fn(i % n_sets)
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for i in range(steps):
+        fn(i % n_sets)
+    end.record(stream)
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) / steps  # ms per launch
+
+
+def cpu_baseline(x_rows, d, budget_s=10.0):
+    """The oracle as it stands, single-threaded, on the first rows of the same
+    workload until about budget_s of CPU time has been spent."""
+    import oracle
+    oracle.mxnorm_mxfp8(x_rows[:4])   # builds/loads the library outside the timing
+    done = 0
+    t0 = time.perf_counter()
+    step = 512
+    while done < x_rows.shape[0] and time.perf_counter() - t0 < budget_s:
+        oracle.mxnorm_mxfp8(x_rows[done:done + step])
+        done += step
+    el = time.perf_counter() - t0
+    return {
+        "value": round(mxfp8_bytes(done, d) / el / 1e9, 4),
+        "unit": "GB/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": "first %d rows of %s (%d elements), single-threaded C oracle, %.1f s"
+                  % (done, WORKLOAD, done * d, el),
+        "rows_per_s": round(done / el, 1),
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path "
+              "(rows are independent; see the sharding notes).  Run with --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2603_13180_amd import mxnorm, synth
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    mxnorm.load()
+
+    w = synth.generate(WORKLOAD)
+    T, d = w.preset.T, w.preset.d
+    x0 = torch.from_numpy(w.x.view(np.int16)).view(torch.bfloat16).to(dev)
+    g = torch.from_numpy(w.gamma.view(np.int16)).view(torch.bfloat16).to(dev)
+    n_sets = max(2, -(-ROTATE_MIN_BYTES // x0.numel() // 2))
+    xs = [x0] + [x0.clone() for _ in range(n_sets - 1)]
+    codes = [torch.empty(T, d, dtype=torch.uint8, device=dev) for _ in range(n_sets)]
+    scales = [torch.empty(T, d // 32, dtype=torch.uint8, device=dev) for _ in range(n_sets)]
+    rho = [torch.empty(T, dtype=torch.float32, device=dev) for _ in range(n_sets)]
+    ncodes = [torch.empty(T, d // 2, dtype=torch.uint8, device=dev) for _ in range(n_sets)]
+    nscales = [torch.empty(T, d // 16, dtype=torch.uint8, device=dev) for _ in range(n_sets)]
+    stream = torch.cuda.current_stream(dev)
+
+    def mxn(i):
+        mxnorm.mxnorm_mxfp8_fwd(xs[i], codes=codes[i], scales=scales[i], rho=rho[i])
+
+    def rms(i):
+        mxnorm.rmsnorm_mxfp8_fwd(xs[i], None, codes=codes[i], scales=scales[i], rho=rho[i])
+
+    def rms_g(i):
+        mxnorm.rmsnorm_mxfp8_fwd(xs[i], g, codes=codes[i], scales=scales[i], rho=rho[i])
+
+    s_g = mxnorm.mxnorm_default_global_scale(d, 16, 2)
+    gmax = float(np.abs(synth.bf16_bits_to_f32(w.gamma)).max())
+    s_r = mxnorm.rmsnorm_default_global_scale(d, gmax)
+
+    def nv_mxn(i):
+        mxnorm.mxnorm_nvfp4_fwd(xs[i], s_g, codes=ncodes[i], scales=nscales[i], rho=rho[i])
+
+    def nv_rms(i):
+        mxnorm.rmsnorm_nvfp4_fwd(xs[i], None, mxnorm.rmsnorm_default_global_scale(d, 1.0),
+                                 codes=ncodes[i], scales=nscales[i], rho=rho[i])
+
+    def nv_rms_g(i):
+        mxnorm.rmsnorm_nvfp4_fwd(xs[i], g, s_r, codes=ncodes[i], scales=nscales[i], rho=rho[i])
+
+    # the headline: exactly `steps` timed MXNorm MXFP8 steps
+    ms = time_launches(mxn, n_sets, args.steps, args.warmup, stream)
+    b8 = mxfp8_bytes(T, d)
+    gbps = b8 / (ms * 1e-3) / 1e9
+
+    side_steps = max(20, args.steps // 4)
+    side = {}
+    for name, fn, nbytes in (("rmsnorm_mxfp8", rms, b8), ("rmsnorm_mxfp8_gamma", rms_g, b8 + 2 * d),
+                             ("mxnorm_nvfp4", nv_mxn, nvfp4_bytes(T, d)),
+                             ("rmsnorm_nvfp4", nv_rms, nvfp4_bytes(T, d)),
+                             ("rmsnorm_nvfp4_gamma", nv_rms_g, nvfp4_bytes(T, d) + 2 * d)):
+        m = time_launches(fn, n_sets, side_steps, 5, stream)
+        side[name] = {"ms": round(m, 5), "GB/s": round(nbytes / (m * 1e-3) / 1e9, 1),
+                      "pct_of_peak": round(100 * nbytes / (m * 1e-3) / 1e9 / PEAK_HBM_GBPS, 2)}
+
+    # device-to-device copy of the same input, a practical bandwidth reference
+    dst = torch.empty_like(x0)
+    m = time_launches(lambda i: dst.copy_(xs[i]), n_sets, 50, 5, stream)
+    copy_gbps = 2 * x0.numel() * 2 / (m * 1e-3) / 1e9
+
+    traffic = measured_traffic()
+    line = {
+        "metric": "MXNorm+MXFP8 cast HBM GB/s (% of peak); speedup vs RMSNorm+cast",
+        "value": round(gbps, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": "%s: MXNorm (p=2, B=32, RCEIL) fwd, x bf16 [%d, %d] N(0,1) with 1%% "
+                        "outlier channels x20 -> E4M3 codes + E8M0 scales + rho" % (WORKLOAD, T, d),
+            "tokens": T, "d": d, "block": 32, "p": 2, "scale_mode": "rceil",
+            "rotating_buffer_sets": n_sets,
+        },
+        "pct_of_peak": round(100 * gbps / PEAK_HBM_GBPS, 2),
+        "rows_per_s": round(T / (ms * 1e-3), 1),
+        "speedup_vs_rmsnorm_cast": round(side["rmsnorm_mxfp8"]["ms"] / ms, 4),
+        "speedup_vs_rmsnorm_gamma_cast": round(side["rmsnorm_mxfp8_gamma"]["ms"] / ms, 4),
+        "nvfp4": {
+            "workload": NV_WORKLOAD,
+            "GB/s": side["mxnorm_nvfp4"]["GB/s"],
+            "pct_of_peak": side["mxnorm_nvfp4"]["pct_of_peak"],
+            "speedup_vs_rmsnorm_cast": round(side["rmsnorm_nvfp4"]["ms"] / side["mxnorm_nvfp4"]["ms"], 4),
+            "speedup_vs_rmsnorm_gamma_cast":
+                round(side["rmsnorm_nvfp4_gamma"]["ms"] / side["mxnorm_nvfp4"]["ms"], 4),
+        },
+        "kernels": side,
+        "copy_d2d_GBps": round(copy_gbps, 1),
+        "roofline": {
+            "bound": "hbm",
+            "achieved": round(gbps, 1),
+            "peak": PEAK_HBM_GBPS,
+            "unit": "GB/s",
+            "frac": round(gbps / PEAK_HBM_GBPS, 4),
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": b8,
+        },
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu:
+        line["cpu_baseline"] = cpu_baseline(w.x, d)
+    print(json.dumps(line))
+
+
+if __name__ == "__main__":
+    main()

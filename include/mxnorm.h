@@ -1,0 +1,143 @@
+/*
+ * mxnorm.h -- C ABI of libmxnorm.so: MXNorm and RMSNorm + MX-cast forward
+ * kernels for AMD Instinct MI355X (gfx950).
+ *
+ * Paper: "MXNorm: Reusing MXFP block scales for efficient tensor
+ * normalisation" (McLean et al., arXiv 2603.13180).
+ *
+ * Common conventions for every compute entry point
+ * ------------------------------------------------
+ *  - x is a row-major bf16 matrix [T, d] (T tokens, hidden size d) given as
+ *    a device pointer; gamma is a bf16 vector [d] (device) or NULL.
+ *  - Outputs are device buffers owned by the caller, contiguous row-major:
+ *      MXFP8: codes  uint8 [T, d]       E4M3 codes, one per element
+ *             scales uint8 [T, d/32]    E8M0 scale bytes (value 2^(b-127),
+ *                                       0xFF = NaN), block k = columns
+ *                                       [32k, 32k+32)
+ *      NVFP4: codes  uint8 [T, d/2]     E2M1 codes, two per byte, element 2j
+ *                                       in the low nibble of byte j
+ *             scales uint8 [T, d/16]    E4M3 block scales (0x7F = NaN)
+ *      rho    float [T] or NULL         the per-row inverse RMS (estimate)
+ *    Dequantised value: code * scale (MXFP8), code * scale * global_scale
+ *    (NVFP4).
+ *  - Alignment: x, gamma and codes must be 16-byte aligned; rho 4-byte.
+ *    x must not overlap any output.
+ *  - Every call is asynchronous on `stream` (a hipStream_t; NULL is the
+ *    default stream).  Nothing is allocated, nothing synchronises.
+ *  - Argument errors are detected on the host and returned before any launch;
+ *    nothing is written then.  mx_last_error() gives a description.
+ *  - T == 0 is a valid no-op (the pointers are not used and may be NULL).
+ *  - d must be a multiple of the block size (32 for MXFP8, 16 for NVFP4) and
+ *    at most MXNORM_MAX_D; larger d returns MX_EUNSUPPORTED.
+ *
+ * Semantics fixed where the paper leaves a choice (the same readings the
+ * test oracle follows):
+ *  - rho and the estimate rho~ are computed in double precision from double
+ *    sums and rounded once to float; every quantity that decides a code is
+ *    then computed in IEEE single precision: t = RN(x * rho~).
+ *  - epsilon goes inside the square root: rho~ = (r^2 + eps)^(-1/2).  A zero
+ *    radicand (all-zero row with eps = 0) gives rho~ = 0.
+ *  - Element casts round to nearest-even and saturate (448 for E4M3, 6 for
+ *    E2M1); signs are kept, also on zero.
+ *  - A block whose scale is NaN (non-finite input) has every code equal to
+ *    the input's sign bit with an all-ones magnitude.
+ */
+#ifndef MXNORM_H
+#define MXNORM_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MXNORM_ABI_VERSION 1
+#define MXNORM_MAX_D 32768
+
+typedef enum {
+    MX_OK = 0,
+    MX_EINVAL = 1,        /* a bad argument; nothing was launched */
+    MX_EUNSUPPORTED = 2,  /* valid but outside what is implemented (d too large) */
+    MX_EHIP = 3           /* the HIP runtime reported an error at launch */
+} mx_status;
+
+typedef enum {
+    MX_SCALE_RCEIL = 0,   /* e = smallest integer with amax <= 448 * 2^e */
+    MX_SCALE_FLOOR = 1    /* e = floor(log2 amax) - 8; elements saturate  */
+} mx_scale_mode;
+
+/*
+ * MXNorm, MXFP8 output (Algorithm 2; Sec. 3.4).
+ * Per row t: m~_k = max over the 32 elements of block k of |x|;
+ *   G = ((1/K) sum_k m~_k^p)^(1/p);  r = coef * G;  rho~ = (r^2 + eps)^(-1/2);
+ *   a_k = RN(m~_k * rho~);  e_k from a_k by `scale_mode`, clamped to
+ *   [-127, 127];  scales = e_k + 127;  codes = E4M3(RN(x * rho~) * 2^-e_k).
+ * p: 1 or 2.  coef: the RMS/G ratio; a value <= 0 selects the paper's table
+ * value for 32-element blocks (0.4261 for p = 1, 0.4185 for p = 2).
+ * eps: >= 0, finite.  No gain: it is folded into the next layer's weight
+ * (Sec. 3.7).
+ */
+mx_status mxnorm_mxfp8_fwd(const void *x, int64_t T, int64_t d, int p, float coef, float eps,
+                           int scale_mode, uint8_t *codes, uint8_t *scales, float *rho,
+                           void *stream);
+
+/*
+ * RMSNorm, optional gain, then the MXFP8 cast (Algorithm 1; Sec. 3.1 eq.
+ * (rms) and eq. (gain); Sec. 3.2 eq. (blockscale) and eq. (blockvals)).
+ * rho = ((1/d) sum x^2 + eps)^(-1/2);  y = RN(RN(x * rho) * gamma) (gamma
+ * NULL: y = RN(x * rho));  m_k = max |y| over block k;  e_k from m_k;
+ * codes = E4M3(y * 2^-e_k).
+ */
+mx_status rmsnorm_mxfp8_fwd(const void *x, const void *gamma, int64_t T, int64_t d, float eps,
+                            int scale_mode, uint8_t *codes, uint8_t *scales, float *rho,
+                            void *stream);
+
+/*
+ * MXNorm with NVFP4 output: 16-element blocks, E4M3 block scales, a float
+ * tensor decode scale global_scale (s_g), E2M1 codes.  rho~ as for MXFP8 with
+ * the 16-element-block coefficient (coef <= 0 selects 0.4814 for p = 1,
+ * 0.4688 for p = 2).  Per block: a = RN(m~ * rho~);  q = a / RN(6 s_g);
+ * S = E4M3(q);  den = RN(dec(S) * s_g);  codes = E2M1(RN(RN(x * rho~) / den)),
+ * or signed zeros when den == 0.
+ * global_scale: finite, >= FLT_MIN and <= FLT_MAX / 6.  The paper uses NVFP4
+ * in its kernel and layer benchmarks (Sec. 4.4); the format's conventions
+ * here are this library's.
+ */
+mx_status mxnorm_nvfp4_fwd(const void *x, int64_t T, int64_t d, int p, float coef, float eps,
+                           float global_scale, uint8_t *codes, uint8_t *scales, float *rho,
+                           void *stream);
+
+/* RMSNorm (+ optional gain) then the NVFP4 cast, as above with y for t. */
+mx_status rmsnorm_nvfp4_fwd(const void *x, const void *gamma, int64_t T, int64_t d, float eps,
+                            float global_scale, uint8_t *codes, uint8_t *scales, float *rho,
+                            void *stream);
+
+/*
+ * Default NVFP4 tensor decode scales: an output bound divided by 6 * 448, so
+ * the bound maps to the largest E2M1 x E4M3 magnitude.  MXNorm: Lemma 2's
+ * bound K^(1/p) / coef (K = d / block; coef <= 0 selects the table value);
+ * RMSNorm: Lemma 1's bound sqrt(d), times max |gamma|.  Sec. 3.5.
+ * Return NaN for invalid arguments.
+ */
+float mxnorm_default_global_scale(int64_t d, int block, int p, float coef);
+float rmsnorm_default_global_scale(int64_t d, float gamma_absmax);
+
+/* The paper's absmax_scale_factor table (implementation appendix): block in
+ * {16, 32, 64}, p in {1, 2}; NaN otherwise. */
+float mxnorm_coef(int block, int p);
+
+/* Static description of a status code. */
+const char *mx_status_str(mx_status s);
+
+/* Description of the last non-OK status returned on the calling thread
+ * ("" if none).  The pointer stays valid until the next call on the thread. */
+const char *mx_last_error(void);
+
+/* MXNORM_ABI_VERSION of the built library. */
+int mxnorm_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MXNORM_H */

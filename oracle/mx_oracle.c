@@ -114,18 +114,26 @@ double mxo_e8m0_value(uint8_t byte)
  * non-negative finite codes; a tie picks the even code (the one whose
  * mantissa LSB is zero), which is IEEE round-half-to-even.  Magnitudes at or
  * above the largest finite value saturate to it (R5). */
+static double e4m3_table[0x7F]; /* values of codes 0x00..0x7E */
+static int e4m3_table_ready = 0;
+
 uint8_t mxo_e4m3_encode(float v)
 {
     uint8_t s = signbit(v) ? 0x80 : 0x00;
     double a, bestd = INFINITY;
     int c, best = 0;
+    if (!e4m3_table_ready) {
+        for (c = 0; c <= 0x7E; c++)
+            e4m3_table[c] = mxo_e4m3_value((uint8_t)c);
+        e4m3_table_ready = 1;
+    }
     if (isnan(v))
         return (uint8_t)(s | 0x7F);
     a = fabs((double)v);
     if (a >= 448.0)
         return (uint8_t)(s | 0x7E);
     for (c = 0; c <= 0x7E; c++) {
-        double dist = fabs(mxo_e4m3_value((uint8_t)c) - a);
+        double dist = fabs(e4m3_table[c] - a);
         if (dist < bestd || (dist == bestd && (c & 1) == 0)) {
             bestd = dist;
             best = c;

@@ -1,0 +1,662 @@
+// mxnorm.hip -- MXNorm and RMSNorm + MX-cast forward kernels for gfx950
+// (AMD Instinct MI355X), behind the C ABI declared in include/mxnorm.h.
+//
+// Paper: "MXNorm: Reusing MXFP block scales for efficient tensor
+// normalisation" (McLean et al., arXiv 2603.13180): Algorithm 1 (RMSNorm +
+// MXCast), Algorithm 2 (MXNorm), Sec. 3.1-3.4.
+//
+// Kernel design (one launch = one pass over the activations):
+//  * A row of d bf16 values is split into 16-byte chunks (8 elements).  A
+//    "team" of TL lanes owns a row; lane l holds chunks j*TL + l, j < CPL, so
+//    every wave-wide load and store is fully coalesced and the whole row stays
+//    in registers between the statistics pass and the cast.  TL is 16, 32 or
+//    64 lanes inside one wave, or 2/4/8 waves (LDS joins their partial sums).
+//  * A scale block (32 elements for MXFP8, 16 for NVFP4) is 4 (2) consecutive
+//    lanes' chunks, so its absmax is a lane-local max plus 2 (1) DPP
+//    quad-permute steps.  MXNorm takes the absmax on the raw bf16 bits (an
+//    unsigned 16-bit max of the magnitudes); the RMSNorm baseline has to form
+//    y = x * rho first and take the absmax of y.
+//  * The row statistic (sum of squared block absmaxes for MXNorm: K terms;
+//    sum of squared elements for RMSNorm: d terms) is accumulated in double
+//    and reduced across the team; rho is computed once per row in double and
+//    rounded to float.  Everything that decides a code is single precision.
+//  * No MFMA: the work is a streaming reduction plus an element-wise cast,
+//    bound by HBM bandwidth.
+#include <hip/hip_runtime.h>
+
+#include <float.h>
+#include <math.h>
+#include <stdarg.h>
+#include <stdint.h>
+#include <stdio.h>
+
+#include "mxnorm.h"
+
+#pragma clang fp contract(off)
+
+namespace {
+
+struct Args {
+    const uint16_t *x;
+    const uint16_t *gamma;
+    uint8_t *codes;
+    uint8_t *scales;
+    float *rho;
+    int64_t T;
+    int d;      // hidden size
+    int nc;     // 16-byte chunks per row (d / 8)
+    int K;      // scale blocks per row
+    int p;      // p-mean exponent (1 or 2)
+    float coef; // RMS / G_p ratio
+    float eps;
+    int mode;   // MX_SCALE_RCEIL or MX_SCALE_FLOOR
+    float s_g;  // NVFP4 tensor decode scale
+};
+
+// ---------------------------------------------------------------- helpers --
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// DPP quad permutes: lane i reads lane i^1 (0xB1 = [1,0,3,2]) or i^2
+// (0x4E = [2,3,0,1]).  Every call site runs with all lanes active.
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_quad(uint32_t v)
+{
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
+}
+
+typedef unsigned short ushort2_t __attribute__((ext_vector_type(2)));
+
+// Largest |x| of 8 bf16 values as the 15-bit magnitude pattern.  Unsigned
+// order of bf16 magnitudes is numeric order, with NaN above Inf, so a NaN
+// input propagates.
+__device__ __forceinline__ uint32_t chunk_absmax_bits(uint4 v)
+{
+    const uint32_t m = 0x7FFF7FFFu;
+    ushort2_t a = __builtin_bit_cast(ushort2_t, v.x & m);
+    ushort2_t b = __builtin_bit_cast(ushort2_t, v.y & m);
+    ushort2_t c = __builtin_bit_cast(ushort2_t, v.z & m);
+    ushort2_t d = __builtin_bit_cast(ushort2_t, v.w & m);
+    ushort2_t r = __builtin_elementwise_max(__builtin_elementwise_max(a, b),
+                                            __builtin_elementwise_max(c, d));
+    return r.x > r.y ? (uint32_t)r.x : (uint32_t)r.y;
+}
+
+// E8M0 scale of a block whose largest |value| is a (>= 0 or NaN): returns the
+// byte e + 127 (0xFF when a is not finite) and 2^-e as a float.
+// RCEIL: the smallest e with a <= 448 * 2^e, i.e. floor(log2 a) - 8, plus one
+// when a's significand exceeds 1.75.  FLOOR: floor(log2 a) - 8.  Both are
+// clamped below at -127 (zero and fp32-subnormal a included); the largest
+// finite a gives e = 120, so no upper clamp is reached and 2^-e is normal.
+__device__ __forceinline__ uint32_t e8m0_scale(float a, int mode, float &inv_scale)
+{
+    const uint32_t ab = __float_as_uint(a) & 0x7FFFFFFFu;
+    const int E = (int)(ab >> 23);
+    if (E == 0xFF) {
+        inv_scale = 0.0f;
+        return 0xFFu;
+    }
+    int e = E - 135;
+    if (mode == MX_SCALE_RCEIL)
+        e += ((ab & 0x7FFFFFu) > 0x600000u) ? 1 : 0;
+    if (E == 0 || e < -127)
+        e = -127;
+    inv_scale = __uint_as_float((uint32_t)(127 - e) << 23);
+    return (uint32_t)(e + 127);
+}
+
+// OCP E4M3 code of v, round to nearest even, saturating at 448; NaN -> 0x7F
+// with v's sign.  Normal range: round the fp32 significand to 3 bits on the
+// integer pattern and rebias the exponent (127 -> 7).  Below 2^-6 the value
+// is n * 2^-9: n = rint(|v| * 512), where n = 8 is the smallest normal code.
+__device__ __forceinline__ uint32_t e4m3_code(float v)
+{
+    const uint32_t u = __float_as_uint(v);
+    const uint32_t s = (u >> 24) & 0x80u;
+    const uint32_t a = u & 0x7FFFFFFFu;
+    uint32_t r;
+    if (a >= 0x43E00000u)
+        r = (a > 0x7F800000u) ? 0x7Fu : 0x7Eu;
+    else if (a >= 0x3C800000u)
+        r = ((a + 0x7FFFFu + ((a >> 20) & 1u)) >> 20) - 0x3C0u;
+    else
+        r = (uint32_t)__builtin_rintf(__uint_as_float(a) * 512.0f);
+    return s | r;
+}
+
+// E2M1 code (low nibble) of |v| with the sign bit of `sign_src`, nearest
+// even, saturating at 6 (a NaN magnitude, which only an overflowed quotient
+// produces here, saturates too).  [1, 6): round the significand to 1 bit and
+// rebias (127 -> 1); below 1 the value is n * 0.5 with n = rint(2 |v|).
+__device__ __forceinline__ uint32_t e2m1_code(float v, float sign_src)
+{
+    const uint32_t s = (__float_as_uint(sign_src) >> 28) & 0x8u;
+    const uint32_t a = __float_as_uint(v) & 0x7FFFFFFFu;
+    uint32_t r;
+    if (a >= 0x40C00000u)
+        r = 7u;
+    else if (a >= 0x3F800000u)
+        r = ((a + 0x1FFFFFu + ((a >> 22) & 1u)) >> 22) - 0xFCu;
+    else
+        r = (uint32_t)__builtin_rintf(__uint_as_float(a) * 2.0f);
+    return s | r;
+}
+
+// Value of a non-negative finite E4M3 code.
+__device__ __forceinline__ float e4m3_value(uint32_t S)
+{
+    const uint32_t E = S >> 3, M = S & 7u;
+    return E ? __uint_as_float(((E + 120u) << 23) | (M << 20)) : (float)M * 0x1p-9f;
+}
+
+// Correctly rounded t / den from the correctly rounded reciprocal r = 1/den:
+// one product and one fused correction (Markstein).  Exact for den >= 2^-90
+// whenever |t / den| >= 2^-20; smaller quotients are below every E2M1 and
+// E4M3 rounding threshold, so the code is unaffected.
+__device__ __forceinline__ float div_by_recip(float t, float den, float r)
+{
+    const float q0 = t * r;
+    const float rem = __builtin_fmaf(-q0, den, t);
+    return __builtin_fmaf(rem, r, q0);
+}
+
+// Codes of a NaN block: each element's bf16 sign bit with an all-ones
+// magnitude.  w0, w1 hold four bf16 values (elements 0..3).
+__device__ __forceinline__ uint32_t nan_codes_e4m3(uint32_t w0, uint32_t w1)
+{
+    return 0x7F7F7F7Fu | ((w0 >> 8) & 0x80u) | ((w0 >> 16) & 0x8000u) |
+           ((w1 << 8) & 0x800000u) | (w1 & 0x80000000u);
+}
+
+__device__ __forceinline__ uint32_t sign_nibbles(uint4 v)
+{
+    // bit 15 of bf16 element k -> bit 4k+3
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+    uint32_t r = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        r |= ((w[i] >> 15) & 1u) << (8 * i + 3);
+        r |= ((w[i] >> 31) & 1u) << (8 * i + 7);
+    }
+    return r;
+}
+
+// rho~ = (r^2 + eps)^(-1/2), r = coef * G_p, G_p from the sum S of m~^p over
+// K blocks (Alg. 2; Sec. 3.4).  Double precision, rounded once to float.
+__device__ __forceinline__ float rho_estimate(double S, int K, int p, float coef, float eps)
+{
+    const double G = (p == 1) ? S / (double)K : sqrt(S / (double)K);
+    const double r = (double)coef * G;
+    const double u = r * r + (double)eps;
+    return (u == 0.0) ? 0.0f : (float)(1.0 / sqrt(u));
+}
+
+// rho = ((1/d) sum x^2 + eps)^(-1/2) (Sec. 3.1 eq. (rms)).
+__device__ __forceinline__ float rho_rms(double S, int d, float eps)
+{
+    const double u = S / (double)d + (double)eps;
+    return (u == 0.0) ? 0.0f : (float)(1.0 / sqrt(u));
+}
+
+// Sum of one double per lane over a team of TL lanes.  Butterfly inside the
+// wave (every lane ends with the same bits: each step adds the same two
+// values), then, for multi-wave teams, per-wave partials through LDS.
+template <int TL>
+__device__ __forceinline__ double team_sum(double s, double *red, int tid)
+{
+    constexpr int W = TL < 64 ? TL : 64;
+#pragma unroll
+    for (int off = 1; off < W; off <<= 1)
+        s += __shfl_xor(s, off, W);
+    if constexpr (TL > 64) {
+        constexpr int NW = TL / 64;
+        const int wave = tid >> 6;
+        if ((tid & 63) == 0)
+            red[wave] = s;
+        __syncthreads();
+        const int first = (wave / NW) * NW;
+        double t = 0.0;
+#pragma unroll
+        for (int i = 0; i < NW; ++i)
+            t += red[first + i];
+        s = t;
+    }
+    return s;
+}
+
+// ------------------------------------------------------------------ kernel --
+
+template <int TL>
+struct Team {
+    static constexpr int BLOCK = TL > 256 ? TL : 256;
+    static constexpr int TEAMS = BLOCK / TL; // rows per workgroup
+};
+
+// NV: NVFP4 output (else MXFP8).  MXN: MXNorm (else RMSNorm).  GAM: apply
+// gamma (RMSNorm only).
+template <int TL, int CPL, bool NV, bool MXN, bool GAM>
+__global__ void __launch_bounds__(Team<TL>::BLOCK)
+norm_cast_kernel(Args A)
+{
+    constexpr int BLOCK = Team<TL>::BLOCK;
+    constexpr int TEAMS = Team<TL>::TEAMS;
+    constexpr int BL = NV ? 2 : 4; // lanes (chunks) per scale block
+    __shared__ double red[TL > 64 ? BLOCK / 64 : 1];
+
+    const int tid = threadIdx.x;
+    const int team = tid / TL;
+    const int l = tid - team * TL;
+    const int64_t row = (int64_t)blockIdx.x * TEAMS + team;
+    const bool row_ok = row < A.T;
+    const int64_t rr = row_ok ? row : 0;
+    const uint4 *xr = reinterpret_cast<const uint4 *>(A.x + rr * A.d);
+
+    uint4 v[CPL];
+    bool ok[CPL];
+#pragma unroll
+    for (int j = 0; j < CPL; ++j) {
+        const int c = j * TL + l;
+        ok[j] = row_ok && c < A.nc;
+        v[j] = ok[j] ? xr[c] : make_uint4(0u, 0u, 0u, 0u);
+    }
+    uint4 g[GAM ? CPL : 1];
+    if constexpr (GAM) {
+        const uint4 *gr = reinterpret_cast<const uint4 *>(A.gamma);
+#pragma unroll
+        for (int j = 0; j < CPL; ++j) {
+            const int c = j * TL + l;
+            g[j] = (c < A.nc) ? gr[c] : make_uint4(0u, 0u, 0u, 0u);
+        }
+    }
+
+    // ---- pass 1: the row statistic ----
+    double s = 0.0;
+    uint32_t mb[MXN ? CPL : 1];
+    if constexpr (MXN) {
+#pragma unroll
+        for (int j = 0; j < CPL; ++j) {
+            uint32_t m = chunk_absmax_bits(v[j]);
+            m = max(m, dpp_quad<0xB1>(m));
+            if constexpr (!NV)
+                m = max(m, dpp_quad<0x4E>(m));
+            mb[j] = m;
+            if ((l % BL) == 0 && ok[j]) {
+                const double md = (double)__uint_as_float(m << 16);
+                s += (A.p == 1) ? md : md * md;
+            }
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < CPL; ++j) {
+            const uint32_t w[4] = {v[j].x, v[j].y, v[j].z, v[j].w};
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const double a = (double)bf16_lo(w[i]);
+                const double b = (double)bf16_hi(w[i]);
+                s = __builtin_fma(a, a, s);
+                s = __builtin_fma(b, b, s);
+            }
+        }
+    }
+    s = team_sum<TL>(s, red, tid);
+    const float rho = MXN ? rho_estimate(s, A.K, A.p, A.coef, A.eps) : rho_rms(s, A.d, A.eps);
+    if (row_ok && l == 0 && A.rho)
+        A.rho[row] = rho;
+
+    // ---- pass 2: block scales and element codes ----
+    const float six_sg = 6.0f * A.s_g;
+    const float rcp_six_sg = 1.0f / six_sg;
+    const bool six_sg_ok = six_sg >= 0x1p-90f;
+#pragma unroll
+    for (int j = 0; j < CPL; ++j) {
+        const int c = j * TL + l;
+        const uint32_t w[4] = {v[j].x, v[j].y, v[j].z, v[j].w};
+        float t[8];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            t[2 * i] = bf16_lo(w[i]) * rho;
+            t[2 * i + 1] = bf16_hi(w[i]) * rho;
+        }
+        if constexpr (GAM) {
+            const uint32_t gw[4] = {g[j].x, g[j].y, g[j].z, g[j].w};
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                t[2 * i] = t[2 * i] * bf16_lo(gw[i]);
+                t[2 * i + 1] = t[2 * i + 1] * bf16_hi(gw[i]);
+            }
+        }
+        // block maximum of |t|
+        float a;
+        if constexpr (MXN) {
+            a = __uint_as_float(mb[j] << 16) * rho;
+        } else {
+            uint32_t m = 0;
+#pragma unroll
+            for (int k = 0; k < 8; ++k)
+                m = max(m, __float_as_uint(t[k]) & 0x7FFFFFFFu);
+            m = max(m, dpp_quad<0xB1>(m));
+            if constexpr (!NV)
+                m = max(m, dpp_quad<0x4E>(m));
+            a = __uint_as_float(m);
+        }
+
+        if constexpr (!NV) {
+            float inv;
+            const uint32_t byte = e8m0_scale(a, A.mode, inv);
+            uint32_t lo = 0, hi = 0;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                lo |= e4m3_code(t[k] * inv) << (8 * k);
+                hi |= e4m3_code(t[k + 4] * inv) << (8 * k);
+            }
+            if (byte == 0xFFu) {
+                lo = nan_codes_e4m3(w[0], w[1]);
+                hi = nan_codes_e4m3(w[2], w[3]);
+            }
+            if (ok[j]) {
+                *reinterpret_cast<uint2 *>(A.codes + rr * A.d + (int64_t)c * 8) =
+                    make_uint2(lo, hi);
+                if ((l & 3) == 0)
+                    A.scales[rr * A.K + (c >> 2)] = (uint8_t)byte;
+            }
+        } else {
+            uint32_t S, packed = 0;
+            if (!(a <= FLT_MAX)) { // NaN or Inf block maximum
+                S = 0x7Fu;
+                packed = 0x77777777u | sign_nibbles(v[j]);
+            } else {
+                float q = six_sg_ok ? div_by_recip(a, six_sg, rcp_six_sg) : a / six_sg;
+                if (q != q) // a is finite: a NaN here is an overflowed quotient
+                    q = __builtin_inff();
+                S = e4m3_code(q);
+                const float den = e4m3_value(S) * A.s_g;
+                if (den == 0.0f) {
+#pragma unroll
+                    for (int k = 0; k < 8; ++k)
+                        packed |= ((__float_as_uint(t[k]) >> 31) << 3) << (4 * k);
+                } else if (den >= 0x1p-90f) {
+                    const float r = 1.0f / den;
+#pragma unroll
+                    for (int k = 0; k < 8; ++k)
+                        packed |= e2m1_code(div_by_recip(t[k], den, r), t[k]) << (4 * k);
+                } else {
+#pragma unroll
+                    for (int k = 0; k < 8; ++k)
+                        packed |= e2m1_code(t[k] / den, t[k]) << (4 * k);
+                }
+            }
+            if (ok[j]) {
+                *reinterpret_cast<uint32_t *>(A.codes + rr * (A.d / 2) + (int64_t)c * 4) = packed;
+                if ((l & 1) == 0)
+                    A.scales[rr * A.K + (c >> 1)] = (uint8_t)S;
+            }
+        }
+    }
+}
+
+// ------------------------------------------------------------ host side --
+
+thread_local char g_err[256] = "";
+
+mx_status fail(mx_status st, const char *fmt, ...)
+{
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return st;
+}
+
+bool aligned(const void *p, uintptr_t n) { return ((uintptr_t)p % n) == 0; }
+
+float table_coef(int block, int p)
+{
+    if (p != 1 && p != 2)
+        return NAN;
+    switch (block) {
+    case 16: return p == 1 ? 0.4814f : 0.4688f;
+    case 32: return p == 1 ? 0.4261f : 0.4185f;
+    case 64: return p == 1 ? 0.3852f : 0.3803f;
+    default: return NAN;
+    }
+}
+
+template <int TL, int CPL, bool NV, bool MXN, bool GAM>
+hipError_t launch_one(const Args &A, hipStream_t stream)
+{
+    const int64_t blocks = (A.T + Team<TL>::TEAMS - 1) / Team<TL>::TEAMS;
+    hipLaunchKernelGGL((norm_cast_kernel<TL, CPL, NV, MXN, GAM>), dim3((unsigned)blocks),
+                       dim3(Team<TL>::BLOCK), 0, stream, A);
+    return hipGetLastError();
+}
+
+template <bool NV, bool MXN, bool GAM>
+hipError_t launch_kind(const Args &A, int TL, int CPL, hipStream_t stream)
+{
+#define MXN_CASE(tl)                                                                     \
+    case tl:                                                                             \
+        return CPL == 4 ? launch_one<tl, 4, NV, MXN, GAM>(A, stream)                     \
+                        : launch_one<tl, 8, NV, MXN, GAM>(A, stream);
+    switch (TL) {
+        MXN_CASE(16)
+        MXN_CASE(32)
+        MXN_CASE(64)
+        MXN_CASE(128)
+        MXN_CASE(256)
+        MXN_CASE(512)
+    }
+#undef MXN_CASE
+    return hipErrorInvalidValue;
+}
+
+// Team size: the smallest of 16 .. 512 lanes holding the row in at most 8
+// chunks per lane; 4 chunks per lane when that suffices.
+void pick_team(int nc, int &TL, int &CPL)
+{
+    static const int sizes[] = {16, 32, 64, 128, 256, 512};
+    TL = 0;
+    CPL = 0;
+    for (int s : sizes) {
+        if (nc <= 8 * s) {
+            TL = s;
+            CPL = nc <= 4 * s ? 4 : 8;
+            return;
+        }
+    }
+}
+
+mx_status check_common(const void *x, const void *gamma, int64_t T, int64_t d, int block,
+                       float eps, const uint8_t *codes, const uint8_t *scales, const float *rho)
+{
+    if (T < 0)
+        return fail(MX_EINVAL, "T must be >= 0 (got %lld)", (long long)T);
+    if (T > 0 && (!x || !codes || !scales))
+        return fail(MX_EINVAL, "x, codes and scales must be non-NULL");
+    if (d <= 0 || d % block != 0)
+        return fail(MX_EINVAL, "d must be a positive multiple of %d (got %lld)", block,
+                    (long long)d);
+    if (d > MXNORM_MAX_D)
+        return fail(MX_EUNSUPPORTED, "d = %lld exceeds the supported maximum %d", (long long)d,
+                    MXNORM_MAX_D);
+    if (!(eps >= 0.0f) || !(eps <= FLT_MAX))
+        return fail(MX_EINVAL, "eps must be finite and >= 0");
+    if (!aligned(x, 16) || !aligned(codes, 16) || (gamma && !aligned(gamma, 16)))
+        return fail(MX_EINVAL, "x, gamma and codes must be 16-byte aligned");
+    if (rho && !aligned(rho, 4))
+        return fail(MX_EINVAL, "rho must be 4-byte aligned");
+    if (T > (int64_t)(INT64_MAX / d) || T / 16 > (int64_t)0x7FFFFFFF)
+        return fail(MX_EUNSUPPORTED, "T = %lld is too large", (long long)T);
+    return MX_OK;
+}
+
+mx_status check_global_scale(float s_g)
+{
+    if (!(s_g >= FLT_MIN) || !(s_g <= FLT_MAX / 6.0f))
+        return fail(MX_EINVAL, "global_scale must be finite, >= FLT_MIN and <= FLT_MAX/6");
+    return MX_OK;
+}
+
+mx_status run(Args A, bool nv, bool mxn, void *stream)
+{
+    int TL, CPL;
+    pick_team(A.nc, TL, CPL);
+    if (TL == 0)
+        return fail(MX_EUNSUPPORTED, "no launch configuration for d = %d", A.d);
+    if (A.T == 0)
+        return MX_OK;
+    hipStream_t st = (hipStream_t)stream;
+    hipError_t e;
+    const bool gam = A.gamma != nullptr;
+    if (!nv && mxn)
+        e = launch_kind<false, true, false>(A, TL, CPL, st);
+    else if (!nv && !mxn)
+        e = gam ? launch_kind<false, false, true>(A, TL, CPL, st)
+                : launch_kind<false, false, false>(A, TL, CPL, st);
+    else if (nv && mxn)
+        e = launch_kind<true, true, false>(A, TL, CPL, st);
+    else
+        e = gam ? launch_kind<true, false, true>(A, TL, CPL, st)
+                : launch_kind<true, false, false>(A, TL, CPL, st);
+    if (e != hipSuccess)
+        return fail(MX_EHIP, "kernel launch failed: %s", hipGetErrorString(e));
+    return MX_OK;
+}
+
+Args make_args(const void *x, const void *gamma, int64_t T, int64_t d, int block, int p,
+               float coef, float eps, int mode, float s_g, uint8_t *codes, uint8_t *scales,
+               float *rho)
+{
+    Args A;
+    A.x = static_cast<const uint16_t *>(x);
+    A.gamma = static_cast<const uint16_t *>(gamma);
+    A.codes = codes;
+    A.scales = scales;
+    A.rho = rho;
+    A.T = T;
+    A.d = (int)d;
+    A.nc = (int)(d / 8);
+    A.K = (int)(d / block);
+    A.p = p;
+    A.coef = coef;
+    A.eps = eps;
+    A.mode = mode;
+    A.s_g = s_g;
+    return A;
+}
+
+mx_status check_p_coef(int p, float &coef, int block)
+{
+    if (p != 1 && p != 2)
+        return fail(MX_EINVAL, "p must be 1 or 2 (got %d)", p);
+    if (isnan(coef) || isinf(coef))
+        return fail(MX_EINVAL, "coef must be finite");
+    if (coef <= 0.0f)
+        coef = table_coef(block, p);
+    return MX_OK;
+}
+
+} // namespace
+
+extern "C" {
+
+mx_status mxnorm_mxfp8_fwd(const void *x, int64_t T, int64_t d, int p, float coef, float eps,
+                           int scale_mode, uint8_t *codes, uint8_t *scales, float *rho,
+                           void *stream)
+{
+    g_err[0] = '\0';
+    mx_status st = check_common(x, nullptr, T, d, 32, eps, codes, scales, rho);
+    if (st != MX_OK)
+        return st;
+    if ((st = check_p_coef(p, coef, 32)) != MX_OK)
+        return st;
+    if (scale_mode != MX_SCALE_RCEIL && scale_mode != MX_SCALE_FLOOR)
+        return fail(MX_EINVAL, "unknown scale_mode %d", scale_mode);
+    return run(make_args(x, nullptr, T, d, 32, p, coef, eps, scale_mode, 1.0f, codes, scales,
+                         rho),
+               false, true, stream);
+}
+
+mx_status rmsnorm_mxfp8_fwd(const void *x, const void *gamma, int64_t T, int64_t d, float eps,
+                            int scale_mode, uint8_t *codes, uint8_t *scales, float *rho,
+                            void *stream)
+{
+    g_err[0] = '\0';
+    mx_status st = check_common(x, gamma, T, d, 32, eps, codes, scales, rho);
+    if (st != MX_OK)
+        return st;
+    if (scale_mode != MX_SCALE_RCEIL && scale_mode != MX_SCALE_FLOOR)
+        return fail(MX_EINVAL, "unknown scale_mode %d", scale_mode);
+    return run(make_args(x, gamma, T, d, 32, 2, 1.0f, eps, scale_mode, 1.0f, codes, scales,
+                         rho),
+               false, false, stream);
+}
+
+mx_status mxnorm_nvfp4_fwd(const void *x, int64_t T, int64_t d, int p, float coef, float eps,
+                           float global_scale, uint8_t *codes, uint8_t *scales, float *rho,
+                           void *stream)
+{
+    g_err[0] = '\0';
+    mx_status st = check_common(x, nullptr, T, d, 16, eps, codes, scales, rho);
+    if (st != MX_OK)
+        return st;
+    if ((st = check_p_coef(p, coef, 16)) != MX_OK)
+        return st;
+    if ((st = check_global_scale(global_scale)) != MX_OK)
+        return st;
+    return run(make_args(x, nullptr, T, d, 16, p, coef, eps, MX_SCALE_RCEIL, global_scale,
+                         codes, scales, rho),
+               true, true, stream);
+}
+
+mx_status rmsnorm_nvfp4_fwd(const void *x, const void *gamma, int64_t T, int64_t d, float eps,
+                            float global_scale, uint8_t *codes, uint8_t *scales, float *rho,
+                            void *stream)
+{
+    g_err[0] = '\0';
+    mx_status st = check_common(x, gamma, T, d, 16, eps, codes, scales, rho);
+    if (st != MX_OK)
+        return st;
+    if ((st = check_global_scale(global_scale)) != MX_OK)
+        return st;
+    return run(make_args(x, gamma, T, d, 16, 2, 1.0f, eps, MX_SCALE_RCEIL, global_scale, codes,
+                         scales, rho),
+               true, false, stream);
+}
+
+float mxnorm_default_global_scale(int64_t d, int block, int p, float coef)
+{
+    if (d <= 0 || (block != 16 && block != 32 && block != 64) || d % block || (p != 1 && p != 2))
+        return NAN;
+    if (!(coef > 0.0f))
+        coef = table_coef(block, p);
+    const double K = (double)(d / block);
+    const double bound = (p == 1 ? K : sqrt(K)) / (double)coef;
+    return (float)(bound / (6.0 * 448.0));
+}
+
+float rmsnorm_default_global_scale(int64_t d, float gamma_absmax)
+{
+    if (d <= 0 || !(gamma_absmax > 0.0f) || !(gamma_absmax <= FLT_MAX))
+        return NAN;
+    return (float)(sqrt((double)d) * (double)gamma_absmax / (6.0 * 448.0));
+}
+
+float mxnorm_coef(int block, int p) { return table_coef(block, p); }
+
+const char *mx_status_str(mx_status s)
+{
+    switch (s) {
+    case MX_OK: return "MX_OK";
+    case MX_EINVAL: return "MX_EINVAL: invalid argument";
+    case MX_EUNSUPPORTED: return "MX_EUNSUPPORTED: unsupported size";
+    case MX_EHIP: return "MX_EHIP: HIP runtime error";
+    }
+    return "unknown mx_status";
+}
+
+const char *mx_last_error(void) { return g_err; }
+
+int mxnorm_abi_version(void) { return MXNORM_ABI_VERSION; }
+
+} // extern "C"

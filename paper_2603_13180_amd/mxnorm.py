@@ -1,0 +1,193 @@
+"""ctypes binding of libmxnorm.so (declared in include/mxnorm.h).
+
+Argument marshalling only: each function checks tensor dtypes, devices and
+shapes, allocates outputs with ``torch.empty`` when none are given, and calls
+the C entry point of the same name on the current HIP stream.  Every step of
+the computation runs in the library's HIP kernels.  There is no fallback: if
+the library is missing, or a tensor is not on the GPU, a call raises.
+"""
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libmxnorm.so")
+
+MX_OK, MX_EINVAL, MX_EUNSUPPORTED, MX_EHIP = 0, 1, 2, 3
+SCALE_MODES = {"rceil": 0, "floor": 1}
+ABI_VERSION = 1
+MAX_D = 32768
+
+_lib = None
+
+
+class MXNormError(RuntimeError):
+    def __init__(self, status, detail):
+        super().__init__("%s (%s)" % (detail, _status_name(status)))
+        self.status = status
+
+
+def _status_name(status):
+    return {0: "MX_OK", 1: "MX_EINVAL", 2: "MX_EUNSUPPORTED", 3: "MX_EHIP"}.get(status, str(status))
+
+
+def load():
+    """Load libmxnorm.so and declare its signatures (no GPU work)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError("libmxnorm.so is not built (expected at %s); run "
+                           "__graft_entry__.build()" % LIB_PATH)
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I64, I, F = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_float
+    sigs = {
+        "mxnorm_mxfp8_fwd": (I, [P, I64, I64, I, F, F, I, P, P, P, P]),
+        "rmsnorm_mxfp8_fwd": (I, [P, P, I64, I64, F, I, P, P, P, P]),
+        "mxnorm_nvfp4_fwd": (I, [P, I64, I64, I, F, F, F, P, P, P, P]),
+        "rmsnorm_nvfp4_fwd": (I, [P, P, I64, I64, F, F, P, P, P, P]),
+        "mxnorm_default_global_scale": (F, [I64, I, I, F]),
+        "rmsnorm_default_global_scale": (F, [I64, F]),
+        "mxnorm_coef": (F, [I, I]),
+        "mx_status_str": (ctypes.c_char_p, [I]),
+        "mx_last_error": (ctypes.c_char_p, []),
+        "mxnorm_abi_version": (I, []),
+    }
+    for name, (res, args) in sigs.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    if lib.mxnorm_abi_version() != ABI_VERSION:
+        raise RuntimeError("libmxnorm.so ABI version %d, binding expects %d"
+                           % (lib.mxnorm_abi_version(), ABI_VERSION))
+    _lib = lib
+    return lib
+
+
+def _check(status):
+    if status != MX_OK:
+        raise MXNormError(status, load().mx_last_error().decode() or "error")
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _input(x):
+    if not isinstance(x, torch.Tensor) or x.dtype != torch.bfloat16 or x.dim() != 2:
+        raise TypeError("x must be a 2-D torch.bfloat16 tensor [T, d]")
+    if not x.is_cuda:
+        raise RuntimeError("x must be on the GPU: libmxnorm has no CPU path")
+    if not x.is_contiguous():
+        raise ValueError("x must be contiguous")
+    return x.shape[0], x.shape[1]
+
+
+def _gamma(gamma, x):
+    if gamma is None:
+        return None
+    if gamma.dtype != torch.bfloat16 or gamma.shape != (x.shape[1],) or gamma.device != x.device:
+        raise TypeError("gamma must be a bfloat16 [d] tensor on x's device")
+    return gamma.contiguous()
+
+
+def _out(t, shape, dtype, device):
+    if t is None:
+        return torch.empty(shape, dtype=dtype, device=device)
+    if t.shape != shape or t.dtype != dtype or t.device != device or not t.is_contiguous():
+        raise ValueError("output tensor must be contiguous %s %s on %s" % (dtype, shape, device))
+    return t
+
+
+def mxnorm_mxfp8_fwd(x, p=2, coef=0.0, eps=1e-6, scale_mode="rceil",
+                     codes=None, scales=None, rho=None, want_rho=True):
+    """MXNorm (Algorithm 2) with MXFP8 output.
+
+    Returns (codes uint8 [T, d] E4M3, scales uint8 [T, d/32] E8M0,
+    rho float32 [T] or None)."""
+    T, d = _input(x)
+    codes = _out(codes, (T, d), torch.uint8, x.device)
+    scales = _out(scales, (T, d // 32), torch.uint8, x.device)
+    if want_rho:
+        rho = _out(rho, (T,), torch.float32, x.device)
+    _check(load().mxnorm_mxfp8_fwd(_ptr(x), T, d, p, coef, eps, SCALE_MODES[scale_mode],
+                                   _ptr(codes), _ptr(scales), _ptr(rho) if want_rho else None,
+                                   _stream(x.device)))
+    return codes, scales, (rho if want_rho else None)
+
+
+def rmsnorm_mxfp8_fwd(x, gamma=None, eps=1e-6, scale_mode="rceil",
+                      codes=None, scales=None, rho=None, want_rho=True):
+    """RMSNorm (+ optional gain) then MXFP8 cast (Algorithm 1)."""
+    T, d = _input(x)
+    g = _gamma(gamma, x)
+    codes = _out(codes, (T, d), torch.uint8, x.device)
+    scales = _out(scales, (T, d // 32), torch.uint8, x.device)
+    if want_rho:
+        rho = _out(rho, (T,), torch.float32, x.device)
+    _check(load().rmsnorm_mxfp8_fwd(_ptr(x), _ptr(g), T, d, eps, SCALE_MODES[scale_mode],
+                                    _ptr(codes), _ptr(scales), _ptr(rho) if want_rho else None,
+                                    _stream(x.device)))
+    return codes, scales, (rho if want_rho else None)
+
+
+def mxnorm_nvfp4_fwd(x, global_scale=None, p=2, coef=0.0, eps=1e-6,
+                     codes=None, scales=None, rho=None, want_rho=True):
+    """MXNorm with NVFP4 output.  global_scale None selects the Lemma-2
+    default.  Returns (packed E2M1 codes uint8 [T, d/2], E4M3 scales uint8
+    [T, d/16], rho)."""
+    T, d = _input(x)
+    if global_scale is None:
+        global_scale = mxnorm_default_global_scale(d, 16, p, coef)
+    codes = _out(codes, (T, d // 2), torch.uint8, x.device)
+    scales = _out(scales, (T, d // 16), torch.uint8, x.device)
+    if want_rho:
+        rho = _out(rho, (T,), torch.float32, x.device)
+    _check(load().mxnorm_nvfp4_fwd(_ptr(x), T, d, p, coef, eps, global_scale, _ptr(codes),
+                                   _ptr(scales), _ptr(rho) if want_rho else None,
+                                   _stream(x.device)))
+    return codes, scales, (rho if want_rho else None)
+
+
+def rmsnorm_nvfp4_fwd(x, gamma=None, global_scale=None, eps=1e-6,
+                      codes=None, scales=None, rho=None, want_rho=True):
+    T, d = _input(x)
+    g = _gamma(gamma, x)
+    if global_scale is None:
+        if g is not None:
+            raise ValueError("pass global_scale when gamma is given; "
+                             "rmsnorm_default_global_scale(d, max|gamma|) is the Lemma-1 default")
+        global_scale = rmsnorm_default_global_scale(d, 1.0)
+    codes = _out(codes, (T, d // 2), torch.uint8, x.device)
+    scales = _out(scales, (T, d // 16), torch.uint8, x.device)
+    if want_rho:
+        rho = _out(rho, (T,), torch.float32, x.device)
+    _check(load().rmsnorm_nvfp4_fwd(_ptr(x), _ptr(g), T, d, eps, global_scale, _ptr(codes),
+                                    _ptr(scales), _ptr(rho) if want_rho else None,
+                                    _stream(x.device)))
+    return codes, scales, (rho if want_rho else None)
+
+
+def mxnorm_default_global_scale(d, block=16, p=2, coef=0.0):
+    return float(load().mxnorm_default_global_scale(d, block, p, coef))
+
+
+def rmsnorm_default_global_scale(d, gamma_absmax=1.0):
+    return float(load().rmsnorm_default_global_scale(d, gamma_absmax))
+
+
+def mxnorm_coef(block, p):
+    return float(load().mxnorm_coef(block, p))
+
+
+def mx_status_str(status):
+    return load().mx_status_str(status).decode()
+
+
+def mx_last_error():
+    return load().mx_last_error().decode()

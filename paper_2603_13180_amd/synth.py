@@ -20,6 +20,7 @@ Recipe (every preset):
     then the gain;
   * float32 values are rounded to bf16 with round-to-nearest-even.
 """
+from concurrent.futures import ThreadPoolExecutor
 from dataclasses import dataclass, field
 
 import numpy as np
@@ -31,10 +32,12 @@ AUX = 1 << 30
 def f32_to_bf16_bits(x):
     """Round float32 values to bf16 (nearest, ties to even); NaN stays NaN."""
     x = np.ascontiguousarray(x, dtype=np.float32)
-    u = x.view(np.uint32).astype(np.uint64)
-    rounded = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
-    out = rounded.astype(np.uint16)
+    u = x.view(np.uint32)
     nan = np.isnan(x)
+    # no uint32 overflow: finite and infinite patterns are <= 0xFF800000
+    r = np.where(nan, np.uint32(0), u)
+    r = (r + ((r >> 16) & 1) + np.uint32(0x7FFF)) >> 16
+    out = r.astype(np.uint16)
     if nan.any():
         out[nan] = ((u[nan] >> 16) | 0x40).astype(np.uint16)
     return out
@@ -110,7 +113,14 @@ def _draw_chunk(preset, seed, c, aux):
         elif preset.kind == "gauss_outlier":
             x[:, aux["outlier_channels"]] *= np.float32(20.0)
     elif preset.kind == "t3_stress":
-        x = (rng.standard_t(3, (n, d)) / np.sqrt(3.0)).astype(np.float32)
+        # Student t with 3 degrees of freedom, Z / sqrt(V / 3) with V the sum
+        # of three squared normals, scaled by 1/sqrt(3) to unit variance
+        z = rng.standard_normal((n, d), dtype=np.float32)
+        v = np.zeros((n, d), np.float32)
+        for _ in range(3):
+            w = rng.standard_normal((n, d), dtype=np.float32)
+            v += w * w
+        x = z / np.sqrt(v)
         hit = rng.random((n, d)) < 0.001
         sign = np.where(rng.random((n, d)) < 0.5, -1.0, 1.0).astype(np.float32)
         x[hit] = 448.0 * sign[hit]
@@ -145,10 +155,15 @@ def generate(name, seed=0, rows=None):
         raise ValueError("row index out of range")
     out = np.empty((rows.size, preset.d), np.uint16)
     chunks = np.unique(rows // CHUNK)
-    for c in chunks:
+
+    def fill(c):
         x = _draw_chunk(preset, seed, int(c), aux)
         sel = np.nonzero(rows // CHUNK == c)[0]
         out[sel] = f32_to_bf16_bits(x[rows[sel] - c * CHUNK])
+
+    # chunks are independent streams; threads only change the wall time
+    with ThreadPoolExecutor(max_workers=min(8, len(chunks)) or 1) as ex:
+        list(ex.map(fill, chunks))
     return Workload(preset, out, f32_to_bf16_bits(aux["gamma"]), rows)
 
 

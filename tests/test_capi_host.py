@@ -1,0 +1,129 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads, exports
+every function include/mxnorm.h declares, and rejects bad arguments on the
+host -- before any launch and without touching the GPU."""
+import ctypes
+import math
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2603_13180_amd import mxnorm
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mxnorm.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(mxnorm.LIB_PATH),
+                                reason="libmxnorm.so not built")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b([a-z_][a-z0-9_]*)\s*\(", text)) - {"defined"})
+
+
+def test_library_exports_every_declared_function():
+    names = declared_functions()
+    assert len(names) >= 10
+    lib = ctypes.CDLL(mxnorm.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) >= {"mxnorm_mxfp8_fwd", "rmsnorm_mxfp8_fwd", "mxnorm_nvfp4_fwd",
+                          "rmsnorm_nvfp4_fwd"}
+
+
+def test_header_compiles_as_c():
+    import subprocess
+    import tempfile
+    with tempfile.TemporaryDirectory() as d:
+        src = os.path.join(d, "t.c")
+        open(src, "w").write('#include "mxnorm.h"\nint main(void){return MX_OK;}\n')
+        subprocess.run(["gcc", "-std=c99", "-Wall", "-Werror", "-I", os.path.dirname(HEADER),
+                        "-c", src, "-o", os.path.join(d, "t.o")], check=True)
+
+
+def test_abi_version_status_strings_and_coefs():
+    lib = mxnorm.load()
+    assert lib.mxnorm_abi_version() == 1
+    for s in range(4):
+        assert mxnorm.mx_status_str(s).startswith("MX_")
+    assert mxnorm.mxnorm_coef(32, 2) == np.float32(0.4185)
+    assert mxnorm.mxnorm_coef(16, 1) == np.float32(0.4814)
+    assert math.isnan(mxnorm.mxnorm_coef(8, 2)) and math.isnan(mxnorm.mxnorm_coef(32, 3))
+
+
+def test_default_global_scales_match_oracle():
+    import oracle
+    for d in (1024, 4096, 768 * 2):
+        for p in (1, 2):
+            assert mxnorm.mxnorm_default_global_scale(d, 16, p) == \
+                np.float32(oracle.mxnorm_default_global_scale(d, 16, p))
+        assert mxnorm.rmsnorm_default_global_scale(d, 1.5) == \
+            np.float32(oracle.rmsnorm_default_global_scale(d, 1.5))
+    assert math.isnan(mxnorm.mxnorm_default_global_scale(100, 16, 2))
+    assert math.isnan(mxnorm.rmsnorm_default_global_scale(64, -1.0))
+
+
+# Fake host pointers: validation must reject the call before it could be
+# dereferenced, launched or written to.
+A16 = 0x10000
+A8 = 0x10008
+OUT = 0x20000
+
+
+def mxfp8(lib, x=A16, T=4, d=64, p=2, coef=0.0, eps=1e-6, mode=0, codes=OUT, scales=OUT,
+          rho=None):
+    return lib.mxnorm_mxfp8_fwd(x, T, d, p, coef, eps, mode, codes, scales, rho, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(x=None), 1), (dict(codes=None), 1), (dict(scales=None), 1),
+    (dict(T=-1), 1), (dict(d=0), 1), (dict(d=48), 1), (dict(d=65536), 2),
+    (dict(p=3), 1), (dict(p=0), 1), (dict(coef=float("nan")), 1), (dict(coef=float("inf")), 1),
+    (dict(eps=-1.0), 1), (dict(eps=float("nan")), 1), (dict(eps=float("inf")), 1),
+    (dict(mode=2), 1), (dict(x=A8), 1), (dict(codes=OUT + 4), 1), (dict(rho=OUT + 2), 1),
+])
+def test_mxnorm_mxfp8_rejects_bad_arguments(kw, status):
+    lib = mxnorm.load()
+    assert mxfp8(lib, **kw) == status
+    assert mxnorm.mx_last_error() != ""
+
+
+def test_zero_rows_is_a_no_op_without_launch():
+    lib = mxnorm.load()
+    assert mxfp8(lib, T=0) == 0
+    assert lib.rmsnorm_mxfp8_fwd(A16, None, 0, 64, 1e-6, 0, OUT, OUT, None, None) == 0
+    assert lib.mxnorm_nvfp4_fwd(A16, 0, 64, 2, 0.0, 1e-6, 0.01, OUT, OUT, None, None) == 0
+    assert lib.rmsnorm_nvfp4_fwd(A16, None, 0, 64, 1e-6, 0.01, OUT, OUT, None, None) == 0
+    # an empty tensor may come with NULL data pointers
+    assert mxfp8(lib, x=None, T=0, codes=None, scales=None) == 0
+    assert lib.mxnorm_nvfp4_fwd(None, 0, 64, 2, 0.0, 1e-6, 0.01, None, None, None, None) == 0
+    # shape and scalar arguments are still checked
+    assert mxfp8(lib, x=None, T=0, d=48, codes=None, scales=None) == 1
+
+
+@pytest.mark.parametrize("sg", [0.0, -1.0, float("nan"), float("inf"), 1e-39, 1e38])
+def test_nvfp4_rejects_bad_global_scale(sg):
+    lib = mxnorm.load()
+    assert lib.mxnorm_nvfp4_fwd(A16, 4, 64, 2, 0.0, 1e-6, sg, OUT, OUT, None, None) == 1
+    assert lib.rmsnorm_nvfp4_fwd(A16, None, 4, 64, 1e-6, sg, OUT, OUT, None, None) == 1
+
+
+def test_nvfp4_and_rmsnorm_shape_rules():
+    lib = mxnorm.load()
+    # NVFP4 needs d % 16 == 0; MXFP8 needs d % 32 == 0
+    assert lib.mxnorm_nvfp4_fwd(A16, 4, 40, 2, 0.0, 1e-6, 0.01, OUT, OUT, None, None) == 1
+    assert lib.rmsnorm_mxfp8_fwd(A16, None, 4, 48, 1e-6, 0, OUT, OUT, None, None) == 1
+    assert lib.rmsnorm_mxfp8_fwd(A16, A8, 4, 64, 1e-6, 0, OUT, OUT, None, None) == 1  # gamma align
+    assert lib.rmsnorm_mxfp8_fwd(A16, None, 4, 64, 1e-6, 5, OUT, OUT, None, None) == 1
+
+
+def test_binding_refuses_cpu_tensors():
+    import torch
+    x = torch.zeros(4, 64, dtype=torch.bfloat16)
+    with pytest.raises(RuntimeError, match="GPU"):
+        mxnorm.mxnorm_mxfp8_fwd(x)
+    with pytest.raises(TypeError):
+        mxnorm.mxnorm_mxfp8_fwd(torch.zeros(4, 64))
