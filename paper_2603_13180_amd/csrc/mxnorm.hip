@@ -51,12 +51,23 @@ struct Args {
     float eps;
     int mode;   // MX_SCALE_RCEIL or MX_SCALE_FLOOR
     float s_g;  // NVFP4 tensor decode scale
+    int sw;     // bytes per scale store: 16, 4 or 1 (set from K and alignment)
 };
 
 // ---------------------------------------------------------------- helpers --
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+
+// Streaming 16-byte load: each input byte is read exactly once, so mark it
+// non-temporal.
+__device__ __forceinline__ uint4 load_stream(const uint4 *p)
+{
+    const u32x4_t t = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(p));
+    return make_uint4(t.x, t.y, t.z, t.w);
+}
 
 // DPP quad permutes: lane i reads lane i^1 (0xB1 = [1,0,3,2]) or i^2
 // (0x4E = [2,3,0,1]).  Every call site runs with all lanes active.
@@ -83,31 +94,42 @@ __device__ __forceinline__ uint32_t chunk_absmax_bits(uint4 v)
     return r.x > r.y ? (uint32_t)r.x : (uint32_t)r.y;
 }
 
-// E8M0 scale of a block whose largest |value| is a (>= 0 or NaN): returns the
-// byte e + 127 (0xFF when a is not finite) and 2^-e as a float.
-// RCEIL: the smallest e with a <= 448 * 2^e, i.e. floor(log2 a) - 8, plus one
-// when a's significand exceeds 1.75.  FLOOR: floor(log2 a) - 8.  Both are
-// clamped below at -127 (zero and fp32-subnormal a included); the largest
-// finite a gives e = 120, so no upper clamp is reached and 2^-e is normal.
-__device__ __forceinline__ uint32_t e8m0_scale(float a, int mode, float &inv_scale)
+// E8M0 scale byte of a block whose largest |value| is a (>= +0 or NaN): e + 127,
+// or 0xFF when a is not finite.  With E the biased fp32 exponent of a and m
+// its 23-bit significand field: RCEIL (the smallest e with a <= 448 * 2^e)
+// is e + 127 = E - 8 + [m > 0x600000], which is ((a + 0x1FFFFF) >> 23) - 8 on
+// the bit pattern; FLOOR (e = floor(log2 a) - 8) is (a >> 23) - 8.  Both are
+// clamped below at byte 0 (e = -127), which also covers zero and fp32
+// subnormals; the largest finite a gives byte 247, so no upper clamp.
+__device__ __forceinline__ uint32_t e8m0_byte(float a, int mode)
 {
-    const uint32_t ab = __float_as_uint(a) & 0x7FFFFFFFu;
-    const int E = (int)(ab >> 23);
-    if (E == 0xFF) {
-        inv_scale = 0.0f;
-        return 0xFFu;
-    }
-    int e = E - 135;
-    if (mode == MX_SCALE_RCEIL)
-        e += ((ab & 0x7FFFFFu) > 0x600000u) ? 1 : 0;
-    if (E == 0 || e < -127)
-        e = -127;
-    inv_scale = __uint_as_float((uint32_t)(127 - e) << 23);
-    return (uint32_t)(e + 127);
+    const uint32_t ab = __float_as_uint(a); // sign bit clear unless a is NaN
+    const uint32_t round = (mode == MX_SCALE_RCEIL) ? 0x1FFFFFu : 0u;
+    const uint32_t biased = (ab + round) >> 23;
+    const uint32_t byte = max(biased, 8u) - 8u;
+    return (ab >= 0x7F800000u) ? 0xFFu : byte;
+}
+
+typedef short short2_t __attribute__((ext_vector_type(2)));
+
+// Four E4M3 codes (one dword, element 0 in the low byte) of t0..t3 / 2^e.
+// v_cvt_scalef32_pk_fp8_f32 divides by 2^(exponent field of the scale
+// operand - 127) and rounds to nearest even; the E8M0 byte shifted into the
+// fp32 exponent field is therefore the scale operand (byte 0 reads as
+// 2^-127).  The instruction returns NaN above 464 instead of saturating, so
+// callers keep |t / 2^e| <= 448: RCEIL guarantees it, FLOOR clamps first.
+// Checked against the software encoder below on all 2^32 fp32 inputs for
+// several exponents, including -127 and 120.
+__device__ __forceinline__ uint32_t e4m3x4_hw(float t0, float t1, float t2, float t3,
+                                              float scale)
+{
+    short2_t r = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32((short2_t){0, 0}, t0, t1, scale, false);
+    r = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(r, t2, t3, scale, true);
+    return __builtin_bit_cast(uint32_t, r);
 }
 
 // OCP E4M3 code of v, round to nearest even, saturating at 448; NaN -> 0x7F
-// with v's sign.  Normal range: round the fp32 significand to 3 bits on the
+// with v's sign (the software encoder; used once per NVFP4 block).  Normal range: round the fp32 significand to 3 bits on the
 // integer pattern and rebias the exponent (127 -> 7).  Below 2^-6 the value
 // is n * 2^-9: n = rint(|v| * 512), where n = 8 is the smallest normal code.
 __device__ __forceinline__ uint32_t e4m3_code(float v)
@@ -235,6 +257,24 @@ struct Team {
 
 // NV: NVFP4 output (else MXFP8).  MXN: MXNorm (else RMSNorm).  GAM: apply
 // gamma (RMSNorm only).
+// Chunks j*TL + l (j < CPL) of `row` into v; zeros outside the tensor.
+template <int TL, int CPL>
+__device__ __forceinline__ void load_row(const Args &A, int64_t row, int l, uint4 (&v)[CPL])
+{
+    const bool row_ok = row < A.T;
+    const uint4 *xr = reinterpret_cast<const uint4 *>(A.x + (row_ok ? row : 0) * A.d);
+#pragma unroll
+    for (int j = 0; j < CPL; ++j) {
+        const int c = j * TL + l;
+        v[j] = (row_ok && c < A.nc) ? load_stream(xr + c) : make_uint4(0u, 0u, 0u, 0u);
+    }
+}
+
+// NV: NVFP4 output (else MXFP8).  MXN: MXNorm (else RMSNorm).  GAM: apply
+// gamma (RMSNorm only).  Workgroup b handles rows b*TEAMS .. b*TEAMS+TEAMS-1,
+// one per team.  (A persistent variant that prefetches each team's next row
+// during the current one needs about twice the registers; at the resulting
+// occupancy it was slower for five of the six kernels on MI355X.)
 template <int TL, int CPL, bool NV, bool MXN, bool GAM>
 __global__ void __launch_bounds__(Team<TL>::BLOCK)
 norm_cast_kernel(Args A)
@@ -243,24 +283,31 @@ norm_cast_kernel(Args A)
     constexpr int TEAMS = Team<TL>::TEAMS;
     constexpr int BL = NV ? 2 : 4; // lanes (chunks) per scale block
     __shared__ double red[TL > 64 ? BLOCK / 64 : 1];
+    // the scale bytes of each row, gathered here and written with wide stores
+    constexpr int KMAX = TL * CPL / BL;
+    __shared__ __attribute__((aligned(16))) uint8_t sbuf[TEAMS * KMAX];
+    // NVFP4: 1 / RN(dec(S) s_g) for every finite E4M3 block scale S, one IEEE
+    // division per entry per workgroup instead of one per block
+    __shared__ float rcp_den[NV ? 128 : 1];
+    float six_sg = 0.0f, rcp_six_sg = 0.0f;
+    bool six_sg_ok = false;
+    if constexpr (NV) {
+        if (threadIdx.x < 127) {
+            const float den = e4m3_value(threadIdx.x) * A.s_g;
+            rcp_den[threadIdx.x] = 1.0f / den;
+        }
+        six_sg = 6.0f * A.s_g;
+        rcp_six_sg = 1.0f / six_sg;
+        six_sg_ok = six_sg >= 0x1p-90f;
+        __syncthreads();
+    }
 
     const int tid = threadIdx.x;
     const int team = tid / TL;
     const int l = tid - team * TL;
-    const int64_t row = (int64_t)blockIdx.x * TEAMS + team;
-    const bool row_ok = row < A.T;
-    const int64_t rr = row_ok ? row : 0;
-    const uint4 *xr = reinterpret_cast<const uint4 *>(A.x + rr * A.d);
+    uint8_t *sb = sbuf + team * KMAX;
 
-    uint4 v[CPL];
-    bool ok[CPL];
-#pragma unroll
-    for (int j = 0; j < CPL; ++j) {
-        const int c = j * TL + l;
-        ok[j] = row_ok && c < A.nc;
-        v[j] = ok[j] ? xr[c] : make_uint4(0u, 0u, 0u, 0u);
-    }
-    uint4 g[GAM ? CPL : 1];
+    uint4 g[GAM ? CPL : 1]; // gamma chunks: the same columns for every row
     if constexpr (GAM) {
         const uint4 *gr = reinterpret_cast<const uint4 *>(A.gamma);
 #pragma unroll
@@ -270,126 +317,185 @@ norm_cast_kernel(Args A)
         }
     }
 
-    // ---- pass 1: the row statistic ----
-    double s = 0.0;
-    uint32_t mb[MXN ? CPL : 1];
-    if constexpr (MXN) {
+    uint4 v[CPL];
+    {
+        const int64_t row = (int64_t)blockIdx.x * TEAMS + team;
+        load_row<TL, CPL>(A, row, l, v);
+        const bool row_ok = row < A.T;
+        const int64_t rr = row_ok ? row : 0;
+        bool ok[CPL];
 #pragma unroll
-        for (int j = 0; j < CPL; ++j) {
-            uint32_t m = chunk_absmax_bits(v[j]);
-            m = max(m, dpp_quad<0xB1>(m));
-            if constexpr (!NV)
-                m = max(m, dpp_quad<0x4E>(m));
-            mb[j] = m;
-            if ((l % BL) == 0 && ok[j]) {
+        for (int j = 0; j < CPL; ++j)
+            ok[j] = row_ok && (j * TL + l) < A.nc;
+
+        // ---- pass 1: the row statistic ----
+        double s = 0.0;
+        uint32_t mb[MXN ? CPL : 1];
+        if constexpr (MXN) {
+#pragma unroll
+            for (int j = 0; j < CPL; ++j) {
+                uint32_t m = chunk_absmax_bits(v[j]);
+                m = max(m, dpp_quad<0xB1>(m));
+                if constexpr (!NV)
+                    m = max(m, dpp_quad<0x4E>(m));
+                mb[j] = m;
+                // every lane of the block adds its term: the sum is BL times
+                // the block sum, removed exactly (BL is a power of two) below
                 const double md = (double)__uint_as_float(m << 16);
                 s += (A.p == 1) ? md : md * md;
             }
-        }
-    } else {
-#pragma unroll
-        for (int j = 0; j < CPL; ++j) {
-            const uint32_t w[4] = {v[j].x, v[j].y, v[j].z, v[j].w};
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const double a = (double)bf16_lo(w[i]);
-                const double b = (double)bf16_hi(w[i]);
-                s = __builtin_fma(a, a, s);
-                s = __builtin_fma(b, b, s);
-            }
-        }
-    }
-    s = team_sum<TL>(s, red, tid);
-    const float rho = MXN ? rho_estimate(s, A.K, A.p, A.coef, A.eps) : rho_rms(s, A.d, A.eps);
-    if (row_ok && l == 0 && A.rho)
-        A.rho[row] = rho;
-
-    // ---- pass 2: block scales and element codes ----
-    const float six_sg = 6.0f * A.s_g;
-    const float rcp_six_sg = 1.0f / six_sg;
-    const bool six_sg_ok = six_sg >= 0x1p-90f;
-#pragma unroll
-    for (int j = 0; j < CPL; ++j) {
-        const int c = j * TL + l;
-        const uint32_t w[4] = {v[j].x, v[j].y, v[j].z, v[j].w};
-        float t[8];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            t[2 * i] = bf16_lo(w[i]) * rho;
-            t[2 * i + 1] = bf16_hi(w[i]) * rho;
-        }
-        if constexpr (GAM) {
-            const uint32_t gw[4] = {g[j].x, g[j].y, g[j].z, g[j].w};
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                t[2 * i] = t[2 * i] * bf16_lo(gw[i]);
-                t[2 * i + 1] = t[2 * i + 1] * bf16_hi(gw[i]);
-            }
-        }
-        // block maximum of |t|
-        float a;
-        if constexpr (MXN) {
-            a = __uint_as_float(mb[j] << 16) * rho;
         } else {
-            uint32_t m = 0;
 #pragma unroll
-            for (int k = 0; k < 8; ++k)
-                m = max(m, __float_as_uint(t[k]) & 0x7FFFFFFFu);
-            m = max(m, dpp_quad<0xB1>(m));
-            if constexpr (!NV)
-                m = max(m, dpp_quad<0x4E>(m));
-            a = __uint_as_float(m);
-        }
-
-        if constexpr (!NV) {
-            float inv;
-            const uint32_t byte = e8m0_scale(a, A.mode, inv);
-            uint32_t lo = 0, hi = 0;
+            for (int j = 0; j < CPL; ++j) {
+                const uint32_t w[4] = {v[j].x, v[j].y, v[j].z, v[j].w};
 #pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                lo |= e4m3_code(t[k] * inv) << (8 * k);
-                hi |= e4m3_code(t[k + 4] * inv) << (8 * k);
-            }
-            if (byte == 0xFFu) {
-                lo = nan_codes_e4m3(w[0], w[1]);
-                hi = nan_codes_e4m3(w[2], w[3]);
-            }
-            if (ok[j]) {
-                *reinterpret_cast<uint2 *>(A.codes + rr * A.d + (int64_t)c * 8) =
-                    make_uint2(lo, hi);
-                if ((l & 3) == 0)
-                    A.scales[rr * A.K + (c >> 2)] = (uint8_t)byte;
-            }
-        } else {
-            uint32_t S, packed = 0;
-            if (!(a <= FLT_MAX)) { // NaN or Inf block maximum
-                S = 0x7Fu;
-                packed = 0x77777777u | sign_nibbles(v[j]);
-            } else {
-                float q = six_sg_ok ? div_by_recip(a, six_sg, rcp_six_sg) : a / six_sg;
-                if (q != q) // a is finite: a NaN here is an overflowed quotient
-                    q = __builtin_inff();
-                S = e4m3_code(q);
-                const float den = e4m3_value(S) * A.s_g;
-                if (den == 0.0f) {
-#pragma unroll
-                    for (int k = 0; k < 8; ++k)
-                        packed |= ((__float_as_uint(t[k]) >> 31) << 3) << (4 * k);
-                } else if (den >= 0x1p-90f) {
-                    const float r = 1.0f / den;
-#pragma unroll
-                    for (int k = 0; k < 8; ++k)
-                        packed |= e2m1_code(div_by_recip(t[k], den, r), t[k]) << (4 * k);
-                } else {
-#pragma unroll
-                    for (int k = 0; k < 8; ++k)
-                        packed |= e2m1_code(t[k] / den, t[k]) << (4 * k);
+                for (int i = 0; i < 4; ++i) {
+                    const double a = (double)bf16_lo(w[i]);
+                    const double b = (double)bf16_hi(w[i]);
+                    s = __builtin_fma(a, a, s);
+                    s = __builtin_fma(b, b, s);
                 }
             }
-            if (ok[j]) {
-                *reinterpret_cast<uint32_t *>(A.codes + rr * (A.d / 2) + (int64_t)c * 4) = packed;
-                if ((l & 1) == 0)
-                    A.scales[rr * A.K + (c >> 1)] = (uint8_t)S;
+        }
+
+
+        // keep the row as raw bf16 between the passes rather than letting
+        // values converted in pass 1 stay live
+#pragma unroll
+        for (int j = 0; j < CPL; ++j)
+            asm volatile("" : "+v"(v[j].x), "+v"(v[j].y), "+v"(v[j].z), "+v"(v[j].w));
+        s = team_sum<TL>(s, red, tid);
+        if constexpr (MXN)
+            s *= 1.0 / BL;
+        const float rho =
+            MXN ? rho_estimate(s, A.K, A.p, A.coef, A.eps) : rho_rms(s, A.d, A.eps);
+        if (row_ok && l == 0 && A.rho)
+            A.rho[row] = rho;
+
+        // ---- pass 2: block scales and element codes ----
+#pragma unroll
+        for (int j = 0; j < CPL; ++j) {
+            const int c = j * TL + l;
+            const uint32_t w[4] = {v[j].x, v[j].y, v[j].z, v[j].w};
+            float t[8];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                t[2 * i] = bf16_lo(w[i]) * rho;
+                t[2 * i + 1] = bf16_hi(w[i]) * rho;
+            }
+            if constexpr (GAM) {
+                const uint32_t gw[4] = {g[j].x, g[j].y, g[j].z, g[j].w};
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    t[2 * i] = t[2 * i] * bf16_lo(gw[i]);
+                    t[2 * i + 1] = t[2 * i + 1] * bf16_hi(gw[i]);
+                }
+            }
+            // block maximum of |t|
+            float a;
+            if constexpr (MXN) {
+                a = __uint_as_float(mb[j] << 16) * rho; // = max |t| (RN is monotone)
+            } else {
+                // integer max of the magnitude patterns: NaN propagates
+                uint32_t m = 0;
+#pragma unroll
+                for (int k = 0; k < 8; ++k)
+                    m = max(m, __float_as_uint(t[k]) & 0x7FFFFFFFu);
+                m = max(m, dpp_quad<0xB1>(m));
+                if constexpr (!NV)
+                    m = max(m, dpp_quad<0x4E>(m));
+                a = __uint_as_float(m);
+            }
+
+            if constexpr (!NV) {
+                const uint32_t byte = e8m0_byte(a, A.mode);
+                if (A.mode == MX_SCALE_FLOOR) {
+                    // |t| <= 448 * 2^e: saturate before the conversion
+                    const float lim = __uint_as_float(((byte + 8u) << 23) | 0x600000u);
+#pragma unroll
+                    for (int k = 0; k < 8; ++k)
+                        t[k] = __builtin_amdgcn_fmed3f(t[k], -lim, lim);
+                }
+                const float scale = __uint_as_float(byte << 23);
+                uint32_t lo = e4m3x4_hw(t[0], t[1], t[2], t[3], scale);
+                uint32_t hi = e4m3x4_hw(t[4], t[5], t[6], t[7], scale);
+                if (__builtin_amdgcn_ballot_w64(byte == 0xFFu)) { // rare: non-finite input
+                    if (byte == 0xFFu) {
+                        lo = nan_codes_e4m3(w[0], w[1]);
+                        hi = nan_codes_e4m3(w[2], w[3]);
+                    }
+                }
+                if (ok[j]) {
+                    *reinterpret_cast<uint2 *>(A.codes + rr * A.d + (int64_t)c * 8) =
+                        make_uint2(lo, hi);
+                    if ((l & 3) == 0)
+                        sb[c >> 2] = (uint8_t)byte;
+                }
+            } else {
+                uint32_t S, packed = 0;
+                if (!(a <= FLT_MAX)) { // NaN or Inf block maximum
+                    S = 0x7Fu;
+                    packed = 0x77777777u | sign_nibbles(v[j]);
+                } else {
+                    float q = six_sg_ok ? div_by_recip(a, six_sg, rcp_six_sg) : a / six_sg;
+                    if (q != q) // a is finite: a NaN here is an overflowed quotient
+                        q = __builtin_inff();
+                    S = e4m3_code(q);
+                    const float den = e4m3_value(S) * A.s_g;
+                    const float r = rcp_den[S];
+                    if (den == 0.0f) {
+#pragma unroll
+                        for (int k = 0; k < 8; ++k)
+                            packed |= ((__float_as_uint(t[k]) >> 31) << 3) << (4 * k);
+                    } else if (den >= 0x1p-90f && a * r <= 0x1p100f) {
+                        // common case: every quotient is finite and the
+                        // Markstein correction is exact; the sign is taken
+                        // from t so zero and underflowing quotients keep it
+                        float vq[8];
+#pragma unroll
+                        for (int k = 0; k < 8; ++k)
+                            vq[k] = __builtin_copysignf(div_by_recip(t[k], den, r), t[k]);
+                        packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, vq[0], vq[1], 1.0f, 0);
+                        packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, vq[2], vq[3], 1.0f, 1);
+                        packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, vq[4], vq[5], 1.0f, 2);
+                        packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, vq[6], vq[7], 1.0f, 3);
+                    } else {
+#pragma unroll
+                        for (int k = 0; k < 8; ++k)
+                            packed |= e2m1_code(t[k] / den, t[k]) << (4 * k);
+                    }
+                }
+                if (ok[j]) {
+                    *reinterpret_cast<uint32_t *>(A.codes + rr * (A.d / 2) + (int64_t)c * 4) =
+                        packed;
+                    if ((l & 1) == 0)
+                        sb[c >> 1] = (uint8_t)S;
+                }
+            }
+        }
+
+        // ---- the row's K scale bytes: LDS -> one wide store per lane ----
+        if constexpr (TL > 64) {
+            __syncthreads();
+        } else {
+            // the team lives in one wave: order its LDS writes before the reads
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        }
+        if (row_ok) {
+            uint8_t *dst = A.scales + rr * A.K;
+            if (A.sw == 16) {
+                if (l < A.K / 16)
+                    *reinterpret_cast<uint4 *>(dst + 16 * l) =
+                        *reinterpret_cast<const uint4 *>(sb + 16 * l);
+            } else if (A.sw == 4) {
+                for (int i = l; i < A.K / 4; i += TL)
+                    *reinterpret_cast<uint32_t *>(dst + 4 * i) =
+                        *reinterpret_cast<const uint32_t *>(sb + 4 * i);
+            } else {
+                for (int i = l; i < A.K; i += TL)
+                    dst[i] = sb[i];
             }
         }
     }
@@ -505,6 +611,10 @@ mx_status run(Args A, bool nv, bool mxn, void *stream)
         return fail(MX_EUNSUPPORTED, "no launch configuration for d = %d", A.d);
     if (A.T == 0)
         return MX_OK;
+    // widest scale store that K and the buffer's alignment allow (K <= 16*TL,
+    // so 16-byte stores need at most one per lane)
+    const uintptr_t sa = (uintptr_t)A.scales;
+    A.sw = (A.K % 16 == 0 && sa % 16 == 0) ? 16 : (A.K % 4 == 0 && sa % 4 == 0) ? 4 : 1;
     hipStream_t st = (hipStream_t)stream;
     hipError_t e;
     const bool gam = A.gamma != nullptr;

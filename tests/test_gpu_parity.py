@@ -348,3 +348,24 @@ def test_device_errors_raise():
     x = torch.zeros(4, 65536, dtype=torch.bfloat16, device=DEV)
     with pytest.raises(mxnorm.MXNormError, match="MX_EUNSUPPORTED"):
         mxnorm.mxnorm_mxfp8_fwd(x)
+
+
+@pytest.mark.parametrize("offset", [1, 4, 8])
+def test_unaligned_scale_pointer(offset):
+    # the library picks 16-, 4- or 1-byte scale stores from K and the pointer
+    T, d = 50, 4096
+    xb = synth.gaussian(T, d, seed=11)
+    x = dev_bf16(xb)
+    for kind, K in (("mxnorm_mxfp8", d // 32), ("mxnorm_nvfp4", d // 16)):
+        buf = torch.full((T * K + 64,), 0xA5, dtype=torch.uint8, device=DEV)
+        scales = buf[offset:offset + T * K].view(T, K)
+        if kind == "mxnorm_mxfp8":
+            c, s, r = mxnorm.mxnorm_mxfp8_fwd(x, scales=scales)
+            want = oracle.mxnorm_mxfp8(xb)
+        else:
+            c, s, r = mxnorm.mxnorm_nvfp4_fwd(x, sg_mxnorm(d), scales=scales)
+            want = oracle.mxnorm_nvfp4(xb, sg_mxnorm(d))
+        torch.cuda.synchronize()
+        b = buf.cpu().numpy()
+        assert np.all(b[:offset] == 0xA5) and np.all(b[offset + T * K:] == 0xA5)
+        assert_parity(kind, (c.cpu().numpy(), s.cpu().numpy(), r.cpu().numpy()), want)
