@@ -1,0 +1,42 @@
+/*
+ * streamref.h -- C ABI of libstreamref.so: a bandwidth reference for the
+ * MXNorm kernels on AMD Instinct MI355X (gfx950).
+ *
+ * mx_stream_reference moves the same HBM bytes with the same access pattern
+ * as mxnorm_mxfp8_fwd (include/mxnorm.h) -- one row of x bf16 [T, d] per
+ * wave, 16-byte loads, 8-byte code stores, one row of d/32 scale bytes staged
+ * in LDS and written with 16-byte stores -- but computes nothing beyond a
+ * byte extraction.  Its throughput is the practical ceiling for that traffic
+ * mix on the device it runs on, the denominator against which the MXNorm
+ * kernels' bandwidth can be judged besides the published HBM peak.
+ *
+ * mode: MX_STREAM_MIXED reads x and writes out [T, d] and out_small
+ *       [T, d/32]; MX_STREAM_READ reads x and writes one 16-byte word per
+ *       row to out_small (which must hold 16*T bytes); MX_STREAM_WRITE
+ *       writes out and out_small without reading x.
+ * d must be a positive multiple of 512 and at most 4096; x, out and
+ * out_small 16-byte aligned device pointers.  Asynchronous on `stream`.
+ * Returns 0 on success, 1 for an invalid argument (nothing launched), 3 if
+ * the launch failed.
+ */
+#ifndef STREAMREF_H
+#define STREAMREF_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MX_STREAM_MIXED 0
+#define MX_STREAM_READ 1
+#define MX_STREAM_WRITE 2
+
+int mx_stream_reference(const void *x, int64_t T, int64_t d, uint8_t *out, uint8_t *out_small,
+                        int mode, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* STREAMREF_H */

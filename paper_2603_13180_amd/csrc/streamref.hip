@@ -1,0 +1,96 @@
+// streamref.hip -- bandwidth reference with the MXNorm kernel's traffic and
+// access pattern and no arithmetic (see include/streamref.h).
+#include <hip/hip_runtime.h>
+
+#include <stdint.h>
+
+#include "streamref.h"
+
+namespace {
+
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint4 load_stream(const uint4 *p)
+{
+    const u32x4_t t = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(p));
+    return make_uint4(t.x, t.y, t.z, t.w);
+}
+
+// One wave per row, rows of nc = d/8 16-byte chunks, nc in {64, 128, ..., 512}.
+template <int MODE>
+__global__ void __launch_bounds__(256) stream_kernel(const uint4 *x, int64_t T, int nc,
+                                                     uint8_t *out, uint8_t *out_small)
+{
+    __shared__ __attribute__((aligned(16))) uint8_t sbuf[4 * 128];
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int64_t row = (int64_t)blockIdx.x * 4 + wave;
+    const bool row_ok = row < T;
+    const int64_t rr = row_ok ? row : 0;
+    const int cpl = nc / 64;
+    uint4 v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        if (MODE == MX_STREAM_WRITE)
+            v[j] = make_uint4((uint32_t)rr, (uint32_t)j, (uint32_t)lane, 1u);
+        else
+            v[j] = (row_ok && j < cpl) ? load_stream(x + rr * nc + j * 64 + lane)
+                                       : make_uint4(0u, 0u, 0u, 0u);
+    }
+    uint8_t *sb = sbuf + wave * 128;
+    if (MODE == MX_STREAM_READ) {
+        uint32_t acc = 0;
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            acc ^= v[j].x ^ v[j].y ^ v[j].z ^ v[j].w;
+        for (int off = 1; off < 64; off <<= 1)
+            acc ^= __shfl_xor(acc, off, 64);
+        if (row_ok && lane == 0)
+            *reinterpret_cast<uint4 *>(out_small + 16 * rr) = make_uint4(acc, 0u, 0u, 0u);
+        return;
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        if (row_ok && j < cpl) {
+            const int c = j * 64 + lane;
+            const uint2 o = make_uint2((v[j].x >> 8) ^ v[j].y, (v[j].z >> 8) ^ v[j].w);
+            *reinterpret_cast<uint2 *>(out + rr * nc * 8 + (int64_t)c * 8) = o;
+            if ((lane & 3) == 0)
+                sb[c >> 2] = (uint8_t)v[j].x;
+        }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    const int K = nc / 4;
+    if (row_ok && lane < K / 16)
+        *reinterpret_cast<uint4 *>(out_small + rr * K + 16 * lane) =
+            *reinterpret_cast<const uint4 *>(sb + 16 * lane);
+}
+
+} // namespace
+
+extern "C" int mx_stream_reference(const void *x, int64_t T, int64_t d, uint8_t *out,
+                                   uint8_t *out_small, int mode, void *stream)
+{
+    if (T < 0 || d <= 0 || d % 512 != 0 || d > 4096 || T > ((int64_t)1 << 34))
+        return 1;
+    if (mode != MX_STREAM_MIXED && mode != MX_STREAM_READ && mode != MX_STREAM_WRITE)
+        return 1;
+    if (T == 0)
+        return 0;
+    if ((mode != MX_STREAM_WRITE && (!x || (uintptr_t)x % 16)) || !out_small ||
+        (uintptr_t)out_small % 16 || (mode != MX_STREAM_READ && (!out || (uintptr_t)out % 16)))
+        return 1;
+    const dim3 grid((unsigned)((T + 3) / 4)), block(256);
+    hipStream_t st = (hipStream_t)stream;
+    const uint4 *xp = static_cast<const uint4 *>(x);
+    const int nc = (int)(d / 8);
+    if (mode == MX_STREAM_MIXED)
+        hipLaunchKernelGGL(stream_kernel<MX_STREAM_MIXED>, grid, block, 0, st, xp, T, nc, out, out_small);
+    else if (mode == MX_STREAM_READ)
+        hipLaunchKernelGGL(stream_kernel<MX_STREAM_READ>, grid, block, 0, st, xp, T, nc, out, out_small);
+    else
+        hipLaunchKernelGGL(stream_kernel<MX_STREAM_WRITE>, grid, block, 0, st, xp, T, nc, out, out_small);
+    return hipGetLastError() == hipSuccess ? 0 : 3;
+}

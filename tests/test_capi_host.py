@@ -18,8 +18,8 @@ pytestmark = pytest.mark.skipif(not os.path.exists(mxnorm.LIB_PATH),
                                 reason="libmxnorm.so not built")
 
 
-def declared_functions():
-    text = open(HEADER).read()
+def declared_functions(header=HEADER):
+    text = open(header).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b([a-z_][a-z0-9_]*)\s*\(", text)) - {"defined"})
 
@@ -32,6 +32,29 @@ def test_library_exports_every_declared_function():
         assert hasattr(lib, n), n
     assert set(names) >= {"mxnorm_mxfp8_fwd", "rmsnorm_mxfp8_fwd", "mxnorm_nvfp4_fwd",
                           "rmsnorm_nvfp4_fwd"}
+
+
+def test_every_header_maps_to_a_library_exporting_it():
+    from paper_2603_13180_amd import streamref
+    libs = {"mxnorm.h": mxnorm.LIB_PATH, "streamref.h": streamref.LIB_PATH}
+    headers = sorted(os.listdir(os.path.dirname(HEADER)))
+    assert set(headers) == set(libs), headers
+    for h in headers:
+        lib = ctypes.CDLL(libs[h])
+        for n in declared_functions(os.path.join(os.path.dirname(HEADER), h)):
+            assert hasattr(lib, n), (h, n)
+
+
+def test_stream_reference_rejects_bad_arguments():
+    from paper_2603_13180_amd import streamref
+    lib = streamref.load()
+    f = lib.mx_stream_reference
+    assert f(A16, 4, 1000, OUT, OUT, 0, None) == 1          # d % 512
+    assert f(A16, 4, 8192, OUT, OUT, 0, None) == 1          # d > 4096
+    assert f(A16, 4, 4096, OUT, OUT, 5, None) == 1          # mode
+    assert f(A8, 4, 4096, OUT, OUT, 0, None) == 1           # alignment
+    assert f(A16, -1, 4096, OUT, OUT, 0, None) == 1
+    assert f(None, 0, 4096, None, None, 0, None) == 0       # T = 0: no-op
 
 
 def test_header_compiles_as_c():
