@@ -37,7 +37,118 @@ def parse():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--sweep", metavar="OUT_JSON",
+                    help="instead of the headline line, run the paper's kernel sweep "
+                         "(17 hidden sizes x 5 token counts) and write per-shape results")
+    ap.add_argument("--sweep-formats", default="mxfp8,nvfp4")
     return ap.parse_args()
+
+
+# the paper's kernel-benchmark grid (appendix "Performance Benchmark Details"):
+# hidden sizes k * 2^r, k in {1, 3, 5, 7}, within [2^10, 2^14]; tokens 2^12 .. 2^16
+SWEEP_D = sorted({k * 2 ** r for k in (1, 3, 5, 7) for r in range(15)
+                  if 1024 <= k * 2 ** r <= 16384})
+SWEEP_T = [4096, 8192, 16384, 32768, 65536]
+
+
+def graph_time(launch, n_sets, reps, rounds, stream):
+    """ms per launch of `launch(i)` for i in 0..n_sets-1, captured once as a
+    HIP graph and replayed `reps` times per round; median over rounds."""
+    import numpy as np
+    import torch
+    for i in range(n_sets):
+        launch(i)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=stream):
+        for i in range(n_sets):
+            launch(i)
+    out = []
+    with torch.cuda.stream(stream):   # replays and events on one stream
+        g.replay()
+        torch.cuda.synchronize()
+        for _ in range(rounds):
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            for _ in range(reps):
+                g.replay()
+            b.record(stream)
+            torch.cuda.synchronize()
+            out.append(a.elapsed_time(b) / (reps * n_sets))
+    del g
+    return float(np.median(out))
+
+
+def run_sweep(path, formats):
+    """Per-shape MXNorm and RMSNorm+cast (both gain-free, as in the paper's
+    kernel benchmark) times and the geometric-mean speedup per format."""
+    import math
+    import numpy as np
+    import torch
+    from paper_2603_13180_amd import mxnorm
+
+    dev = torch.device("cuda:0")
+    mxnorm.load()
+    stream = torch.cuda.Stream(dev)
+    gen = torch.Generator(device=dev)
+    results = []
+    summary = {}
+    for fmt in formats:
+        speedups = []
+        for d in SWEEP_D:
+            for T in SWEEP_T:
+                gen.manual_seed(d * 100003 + T)
+                xbytes = T * d * 2
+                n_sets = max(2, -(-ROTATE_MIN_BYTES // xbytes))
+                x = torch.randn(n_sets, T, d, generator=gen, device=dev).to(torch.bfloat16)
+                if fmt == "mxfp8":
+                    codes = torch.empty(n_sets, T, d, dtype=torch.uint8, device=dev)
+                    scales = torch.empty(n_sets, T, d // 32, dtype=torch.uint8, device=dev)
+                    nbytes = mxfp8_bytes(T, d)
+                    mx = lambda i: mxnorm.mxnorm_mxfp8_fwd(x[i], codes=codes[i], scales=scales[i],
+                                                          want_rho=False)
+                    rm = lambda i: mxnorm.rmsnorm_mxfp8_fwd(x[i], None, codes=codes[i],
+                                                           scales=scales[i], want_rho=False)
+                else:
+                    codes = torch.empty(n_sets, T, d // 2, dtype=torch.uint8, device=dev)
+                    scales = torch.empty(n_sets, T, d // 16, dtype=torch.uint8, device=dev)
+                    nbytes = nvfp4_bytes(T, d) - 4 * T
+                    sg = mxnorm.mxnorm_default_global_scale(d, 16, 2)
+                    sr = mxnorm.rmsnorm_default_global_scale(d, 1.0)
+                    mx = lambda i: mxnorm.mxnorm_nvfp4_fwd(x[i], sg, codes=codes[i], scales=scales[i],
+                                                          want_rho=False)
+                    rm = lambda i: mxnorm.rmsnorm_nvfp4_fwd(x[i], None, sr, codes=codes[i],
+                                                           scales=scales[i], want_rho=False)
+                if fmt == "mxfp8":
+                    nbytes -= 4 * T
+                # about 20 ms of device time per round
+                est_ms = nbytes / 5.0e12 * 1e3
+                reps = max(2, int(20.0 / max(est_ms * n_sets, 1e-3)))
+                t_mx, t_rm = [], []
+                for _ in range(3):    # interleave the two kernels
+                    t_mx.append(graph_time(mx, n_sets, reps, 1, stream))
+                    t_rm.append(graph_time(rm, n_sets, reps, 1, stream))
+                m, r = float(np.median(t_mx)), float(np.median(t_rm))
+                speedups.append(r / m)
+                results.append({"format": fmt, "d": d, "tokens": T, "mxnorm_us": round(m * 1e3, 3),
+                                "rmsnorm_us": round(r * 1e3, 3), "speedup": round(r / m, 4),
+                                "mxnorm_GBps": round(nbytes / (m * 1e-3) / 1e9, 1),
+                                "rmsnorm_GBps": round(nbytes / (r * 1e-3) / 1e9, 1)})
+                print(json.dumps(results[-1]), file=sys.stderr, flush=True)
+                del x, codes, scales
+                torch.cuda.empty_cache()
+        summary[fmt] = {
+            "geomean_speedup": round(math.exp(sum(math.log(v) for v in speedups) / len(speedups)), 4),
+            "min_speedup": round(min(speedups), 4), "max_speedup": round(max(speedups), 4),
+            "shapes": len(speedups)}
+    doc = {"method": "HIP-graph replays of one launch per rotating buffer set (>= 768 MiB of "
+                     "input in rotation), median of 3 interleaved rounds; gain-free kernels, "
+                     "N(0,1) bf16 inputs drawn on the GPU (seeded); bytes = algorithmic bytes",
+           "hidden": SWEEP_D, "tokens": SWEEP_T, "summary": summary, "results": results}
+    with open(path, "w") as f:
+        json.dump(doc, f, indent=1)
+    print(json.dumps({"sweep": path, "summary": summary}))
 
 
 def mxfp8_bytes(T, d):
@@ -110,6 +221,9 @@ def cpu_baseline(x_rows, d, budget_s=10.0):
 
 def main():
     args = parse()
+    if args.sweep:
+        run_sweep(args.sweep, args.sweep_formats.split(","))
+        return
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
               "(rows are independent; see the sharding notes).  Run with --gpus 1.",

@@ -22,6 +22,7 @@ _SRC = os.path.join(_HERE, "mx_oracle.c")
 _LIB = os.path.join(_HERE, "libmx_oracle.so")
 
 SCALE_MODES = {"rceil": 0, "floor": 1}
+ELEMS = {"e4m3": 0, "e2m1": 1}
 MAX_D = 65536
 
 _lib = None
@@ -71,6 +72,10 @@ def _load():
         "mxo_e4m3_encode_array": (None, [P, I64, P]),
         "mxo_e2m1_encode_array": (None, [P, I64, P]),
         "mxo_scale_exponent_array": (None, [P, I64, I, P]),
+        "mxo_scale_exponent_fmt_array": (None, [P, I64, I, I, P]),
+        "mxo_mxcast": (None, [P, I64, I64, I, I, I, P, P]),
+        "mxo_mxnorm_mx": (None, [P, I64, I64, I, I, I, F, F, I, P, P, P, P]),
+        "mxo_rmsnorm_mx": (None, [P, P, I64, I64, I, I, F, I, P, P, P, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -133,10 +138,11 @@ def e2m1_encode(v):
     return out
 
 
-def scale_exponent(a, mode="rceil"):
+def scale_exponent(a, mode="rceil", elem="e4m3"):
     a = np.ascontiguousarray(a, dtype=np.float32)
     out = np.empty(a.shape, np.int32)
-    _load().mxo_scale_exponent_array(_ptr(a), a.size, SCALE_MODES[mode], _ptr(out))
+    _load().mxo_scale_exponent_fmt_array(_ptr(a), a.size, SCALE_MODES[mode], ELEMS[elem],
+                                         _ptr(out))
     return out
 
 
@@ -240,4 +246,55 @@ def rmsnorm_nvfp4(x, s_g, gamma=None, eps=1e-6):
     r64 = np.empty(T, np.float64)
     _load().mxo_rmsnorm_nvfp4(_ptr(x), _ptr(g), T, d, eps, s_g, _ptr(codes), _ptr(scales),
                               _ptr(r32), _ptr(r64))
+    return codes, scales, r32, r64
+
+
+# ------------------------------------------------------- generic MX casts --
+
+def _mx_shapes(T, d, B, elem):
+    if B not in (16, 32, 64) or d % B:
+        raise ValueError("block must be 16, 32 or 64 and divide d")
+    return ((T, d) if elem == "e4m3" else (T, d // 2)), (T, d // B)
+
+
+def mxcast(y, B=32, elem="e4m3", mode="rceil"):
+    """Plain MX cast (eq. blockscale / blockvals) of float32 y [T, d]."""
+    y = np.ascontiguousarray(y, dtype=np.float32)
+    T, d = y.shape
+    cshape, sshape = _mx_shapes(T, d, B, elem)
+    codes = np.empty(cshape, np.uint8)
+    scales = np.empty(sshape, np.uint8)
+    _load().mxo_mxcast(_ptr(y), T, d, B, ELEMS[elem], SCALE_MODES[mode], _ptr(codes),
+                       _ptr(scales))
+    return codes, scales
+
+
+def mxnorm_mx(x, B=32, elem="e4m3", p=2, coef_=None, eps=1e-6, mode="rceil"):
+    """Algorithm 2 with B-element blocks, E8M0 scales and E4M3 or E2M1 codes
+    (E2M1 packed two per byte).  Returns (codes, scales, rho32, rho64)."""
+    x = _as_bf16_rows(x)
+    T, d = x.shape
+    cshape, sshape = _mx_shapes(T, d, B, elem)
+    c = coef(B, p) if coef_ is None else coef_
+    codes = np.empty(cshape, np.uint8)
+    scales = np.empty(sshape, np.uint8)
+    r32 = np.empty(T, np.float32)
+    r64 = np.empty(T, np.float64)
+    _load().mxo_mxnorm_mx(_ptr(x), T, d, B, ELEMS[elem], p, c, eps, SCALE_MODES[mode],
+                          _ptr(codes), _ptr(scales), _ptr(r32), _ptr(r64))
+    return codes, scales, r32, r64
+
+
+def rmsnorm_mx(x, gamma=None, B=32, elem="e4m3", eps=1e-6, mode="rceil"):
+    """Algorithm 1 (RMSNorm, optional gain, then the plain MX cast)."""
+    x = _as_bf16_rows(x)
+    T, d = x.shape
+    cshape, sshape = _mx_shapes(T, d, B, elem)
+    g = _as_gamma(gamma, d)
+    codes = np.empty(cshape, np.uint8)
+    scales = np.empty(sshape, np.uint8)
+    r32 = np.empty(T, np.float32)
+    r64 = np.empty(T, np.float64)
+    _load().mxo_rmsnorm_mx(_ptr(x), _ptr(g), T, d, B, ELEMS[elem], eps, SCALE_MODES[mode],
+                           _ptr(codes), _ptr(scales), _ptr(r32), _ptr(r64))
     return codes, scales, r32, r64

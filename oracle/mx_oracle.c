@@ -30,9 +30,14 @@
  *       rho~ = (r^2 + eps)^(-1/2), rho = (mean x^2 + eps)^(-1/2).  When the
  *       radicand is exactly zero, rho := 0 (the row is all zeros).
  *   R4  E8M0 scale rule: RCEIL -- the smallest integer e with
- *       a <= 448 * 2^e -- or FLOOR: e = floor(log2 a) - 8 (the literal
- *       "divide by 256, round down" reading).  e is clamped to [-127, 127];
- *       byte = e + 127; a non-finite a gives the NaN byte 0xFF.
+ *       a <= max * 2^e, max the element format's largest finite value (448
+ *       for E4M3, 6 for E2M1) -- or FLOOR: e = floor(log2 a) - log2(P), P the
+ *       format's largest power of two (256 for E4M3, 4 for E2M1: the literal
+ *       "divide by P, round down" reading).  e is clamped to [-127, 127];
+ *       byte = e + 127; a non-finite a gives the NaN byte 0xFF.  Block sizes
+ *       16, 32 and 64 and both element formats follow the paper's mx_quantise
+ *       / mx_norm, which take the block size and element dtype as
+ *       parameters.
  *   R5  element casts round to nearest, ties to the even code, and saturate
  *       to the largest finite magnitude (448 for E4M3, 6 for E2M1); the sign
  *       bit is kept, also for zero results.
@@ -162,27 +167,39 @@ uint8_t mxo_e2m1_encode(float v)
     return (uint8_t)(s | best);
 }
 
+/* Element formats of the MX cast (Sec. 3.2; the implementation appendix's
+ * mx_quantise takes the element dtype as a parameter). */
+#define MXO_ELEM_E4M3 0
+#define MXO_ELEM_E2M1 1
+
+/* Largest finite magnitude of the element format. */
+static double elem_max(int elem) { return elem == MXO_ELEM_E2M1 ? 6.0 : 448.0; }
+
+/* log2 of the largest power of two the element format represents
+ * (get_largest_pow2 of the implementation appendix: 256 for E4M3, 4 for
+ * E2M1). */
+static int elem_emax(int elem) { return elem == MXO_ELEM_E2M1 ? 2 : 8; }
+
 /* E8M0 scale exponent for a block whose largest |value| is a (finite,
- * non-negative), Sec. 3.2 eq. (blockscale) with the rounding rule R4.
- * Returns e in [-127, 127]. */
-int mxo_scale_exponent(float a, int mode)
+ * non-negative) and element format elem, Sec. 3.2 eq. (blockscale) with the
+ * rounding rule R4.  Returns e in [-127, 127]. */
+int mxo_scale_exponent_fmt(float a, int mode, int elem)
 {
     int e;
     if (mode == MXO_SCALE_RCEIL) {
-        /* smallest e with a <= 448 * 2^e: 448 * 2^e is exact in double */
+        /* smallest e with a <= max * 2^e: max * 2^e is exact in double */
         e = -127;
-        while (e < 127 && (double)a > ldexp(448.0, e))
+        while (e < 127 && (double)a > ldexp(elem_max(elem), e))
             e++;
         return e;
     }
-    /* FLOOR: e = floor(log2 a) - 8, 256 = 2^8 being the largest power of two
-     * that E4M3 represents */
+    /* FLOOR: e = floor(log2 a) - log2(largest power of two of the format) */
     if (a == 0.0f)
         return -127;
     {
         int E;
         (void)frexp((double)a, &E); /* a = f * 2^E, f in [0.5, 1) */
-        e = (E - 1) - 8;
+        e = (E - 1) - elem_emax(elem);
     }
     if (e < -127)
         e = -127;
@@ -191,15 +208,32 @@ int mxo_scale_exponent(float a, int mode)
     return e;
 }
 
+/* The E4M3 rule (MXFP8). */
+int mxo_scale_exponent(float a, int mode)
+{
+    return mxo_scale_exponent_fmt(a, mode, MXO_ELEM_E4M3);
+}
+
 /* Scale byte of eq. (blockscale): NaN for a non-finite block maximum. */
-static uint8_t e8m0_byte_for(float a, int mode, int *e_out)
+static uint8_t e8m0_byte_for(float a, int mode, int elem, int *e_out)
 {
     if (!isfinite(a)) {
         *e_out = 0;
         return 0xFF;
     }
-    *e_out = mxo_scale_exponent(a, mode);
+    *e_out = mxo_scale_exponent_fmt(a, mode, elem);
     return (uint8_t)(*e_out + 127);
+}
+
+/* Element code (E2M1: in the low nibble) and the NaN-block code (R8). */
+static uint8_t elem_encode(float v, int elem)
+{
+    return elem == MXO_ELEM_E2M1 ? mxo_e2m1_encode(v) : mxo_e4m3_encode(v);
+}
+
+static uint8_t elem_nan_code(int sign, int elem)
+{
+    return elem == MXO_ELEM_E2M1 ? (uint8_t)((sign << 3) | 0x7) : (uint8_t)((sign << 7) | 0x7F);
 }
 
 /* absmax_scale_factor (appendix "Implementation of MXNormLinear"):
@@ -270,61 +304,90 @@ double mxo_rho_from_absmax(const float *m, int64_t K, int p, float coef, float e
 /* MX casts                                                                  */
 /* ------------------------------------------------------------------------ */
 
-/* Plain MXFP8 cast of one block of already-normalised values y (eq.
- * (blockscale), eq. (blockvals)): m = max|y|, S = 2^e, V = E4M3(y / S).
+/* Two E2M1 codes per byte, element 2j in the low nibble of byte j. */
+static void pack_nibbles(const uint8_t *codes, int64_t n, uint8_t *packed)
+{
+    int64_t j;
+    for (j = 0; j < n / 2; j++)
+        packed[j] = (uint8_t)((codes[2 * j] & 0xF) | ((codes[2 * j + 1] & 0xF) << 4));
+}
+
+/* Store one row of per-element codes: bytes for E4M3, packed for E2M1. */
+static void store_row_codes(const uint8_t *rowcodes, int64_t d, int elem, uint8_t *dst)
+{
+    int64_t i;
+    if (elem == MXO_ELEM_E2M1)
+        pack_nibbles(rowcodes, d, dst);
+    else
+        for (i = 0; i < d; i++)
+            dst[i] = rowcodes[i];
+}
+
+/* Plain MX cast of one block of already-normalised values y (eq.
+ * (blockscale), eq. (blockvals)): m = max|y|, S = 2^e, V = cast(y / S).
  * sign_src (bf16 inputs) supplies the sign bits used for NaN blocks (R8);
- * when it is NULL the sign of y is used. */
-static uint8_t mxfp8_cast_block(const float *y, const uint16_t *sign_src, int B, int mode,
-                                uint8_t *codes)
+ * when it is NULL the sign of y is used.  One code per element. */
+static uint8_t mx_cast_block(const float *y, const uint16_t *sign_src, int B, int mode,
+                             int elem, uint8_t *codes)
 {
     float m = block_absmax(y, B);
     int e, b;
-    uint8_t byte = e8m0_byte_for(m, mode, &e);
+    uint8_t byte = e8m0_byte_for(m, mode, elem, &e);
     for (b = 0; b < B; b++) {
         if (byte == 0xFF) {
             int sb = sign_src ? sign_of_bf16(sign_src[b]) : (signbit(y[b]) ? 1 : 0);
-            codes[b] = (uint8_t)((sb << 7) | 0x7F);
+            codes[b] = elem_nan_code(sb, elem);
         } else {
             /* exact power-of-two scaling; a result below the fp32 normal range
-             * is far below E4M3's smallest subnormal and encodes as +-0 */
+             * is far below the smallest subnormal code and encodes as +-0 */
             float v = (float)ldexp((double)y[b], -e);
-            codes[b] = mxo_e4m3_encode(v);
+            codes[b] = elem_encode(v, elem);
         }
     }
     return byte;
 }
 
-/* MXCast of a float matrix [T, d] with 32-element blocks (Sec. 3.2), no
+/* MXCast of a float matrix [T, d] with B-element blocks (Sec. 3.2), no
  * normalisation.  Used to check that MXNorm's cast stage reduces to the plain
- * MX cast. */
+ * MX cast.  codes: [T, d] (E4M3) or [T, d/2] (E2M1). */
+void mxo_mxcast(const float *y, int64_t T, int64_t d, int B, int elem, int mode,
+                uint8_t *codes, uint8_t *scales)
+{
+    int64_t t, k, K = d / B;
+    uint8_t rowcodes[65536];
+    for (t = 0; t < T; t++) {
+        for (k = 0; k < K; k++)
+            scales[t * K + k] = mx_cast_block(y + t * d + k * B, NULL, B, mode, elem,
+                                              rowcodes + k * B);
+        store_row_codes(rowcodes, d, elem, codes + t * (elem == MXO_ELEM_E2M1 ? d / 2 : d));
+    }
+}
+
 void mxo_mxcast_mxfp8(const float *y, int64_t T, int64_t d, int mode, uint8_t *codes,
                       uint8_t *scales)
 {
-    const int B = 32;
-    int64_t t, k, K = d / B;
-    for (t = 0; t < T; t++)
-        for (k = 0; k < K; k++)
-            scales[t * K + k] = mxfp8_cast_block(y + t * d + k * B, NULL, B, mode,
-                                                 codes + t * d + k * B);
+    mxo_mxcast(y, T, d, 32, MXO_ELEM_E4M3, mode, codes, scales);
 }
 
 /* ------------------------------------------------------------------------ */
-/* Algorithm 2: MXNorm, MXFP8 output                                         */
+/* Algorithm 2: MXNorm, MX output (E8M0 scales; E4M3 or E2M1 elements)        */
 /* ------------------------------------------------------------------------ */
 
-/* x: bf16 bits [T, d]; codes: E4M3 [T, d]; scales: E8M0 [T, d/32];
- * rho32 / rho64: the inverse RMS estimate per row (either may be NULL). */
-void mxo_mxnorm_mxfp8(const uint16_t *x, int64_t T, int64_t d, int p, float coef, float eps,
-                      int mode, uint8_t *codes, uint8_t *scales, float *rho32, double *rho64)
+/* x: bf16 bits [T, d]; B-element blocks; codes: E4M3 [T, d] or packed E2M1
+ * [T, d/2]; scales: E8M0 [T, d/B]; rho32 / rho64: the inverse RMS estimate
+ * per row (either may be NULL). */
+void mxo_mxnorm_mx(const uint16_t *x, int64_t T, int64_t d, int B, int elem, int p,
+                   float coef, float eps, int mode, uint8_t *codes, uint8_t *scales,
+                   float *rho32, double *rho64)
 {
-    const int B = 32;
     int64_t K = d / B, t, k;
-    float xf[32];
+    float xf[64];
+    float m[4096];            /* K <= 4096 */
+    uint8_t rowcodes[65536];  /* d <= 65536 */
     for (t = 0; t < T; t++) {
         const uint16_t *xr = x + t * d;
         double rho_d;
         float rho_f;
-        float m[512 * 4]; /* K <= 2048 (d <= 65536) */
         /* step 1: block absmaxes of the raw input */
         for (k = 0; k < K; k++) {
             int b;
@@ -341,21 +404,29 @@ void mxo_mxnorm_mxfp8(const uint16_t *x, int64_t T, int64_t d, int p, float coef
         for (k = 0; k < K; k++) {
             float a = m[k] * rho_f; /* R6: RN32(m~ rho~) */
             int e, b;
-            uint8_t byte = e8m0_byte_for(a, mode, &e);
+            uint8_t byte = e8m0_byte_for(a, mode, elem, &e);
             scales[t * K + k] = byte;
             for (b = 0; b < B; b++) {
                 uint16_t xb = xr[k * B + b];
-                uint8_t *c = codes + t * d + k * B + b;
+                uint8_t *c = rowcodes + k * B + b;
                 if (byte == 0xFF) {
-                    *c = (uint8_t)((sign_of_bf16(xb) << 7) | 0x7F);
+                    *c = elem_nan_code(sign_of_bf16(xb), elem);
                 } else {
                     float tv = mxo_bf16_to_float(xb) * rho_f; /* RN32(x rho~) */
                     float v = (float)ldexp((double)tv, -e);  /* exact */
-                    *c = mxo_e4m3_encode(v);
+                    *c = elem_encode(v, elem);
                 }
             }
         }
+        store_row_codes(rowcodes, d, elem, codes + t * (elem == MXO_ELEM_E2M1 ? d / 2 : d));
     }
+}
+
+/* MXFP8: 32-element blocks, E4M3 elements. */
+void mxo_mxnorm_mxfp8(const uint16_t *x, int64_t T, int64_t d, int p, float coef, float eps,
+                      int mode, uint8_t *codes, uint8_t *scales, float *rho32, double *rho64)
+{
+    mxo_mxnorm_mx(x, T, d, 32, MXO_ELEM_E4M3, p, coef, eps, mode, codes, scales, rho32, rho64);
 }
 
 /* ------------------------------------------------------------------------ */
@@ -363,18 +434,18 @@ void mxo_mxnorm_mxfp8(const uint16_t *x, int64_t T, int64_t d, int p, float coef
 /* ------------------------------------------------------------------------ */
 
 /* y = RN32(RN32(x rho) gamma), gamma optional (Sec. 3.1 eq. (gain)); then the
- * plain MXFP8 cast of eq. (blockscale), eq. (blockvals). */
-void mxo_rmsnorm_mxfp8(const uint16_t *x, const uint16_t *gamma, int64_t T, int64_t d,
-                       float eps, int mode, uint8_t *codes, uint8_t *scales, float *rho32,
-                       double *rho64)
+ * plain MX cast of eq. (blockscale), eq. (blockvals) with B-element blocks. */
+void mxo_rmsnorm_mx(const uint16_t *x, const uint16_t *gamma, int64_t T, int64_t d, int B,
+                    int elem, float eps, int mode, uint8_t *codes, uint8_t *scales,
+                    float *rho32, double *rho64)
 {
-    const int B = 32;
     int64_t K = d / B, t, k, i;
+    float xf[65536];
+    uint8_t rowcodes[65536];
     for (t = 0; t < T; t++) {
         const uint16_t *xr = x + t * d;
         double rho_d;
         float rho_f;
-        float xf[65536];
         for (i = 0; i < d; i++)
             xf[i] = mxo_bf16_to_float(xr[i]);
         rho_d = mxo_rms_inverse(xf, d, eps);
@@ -388,9 +459,17 @@ void mxo_rmsnorm_mxfp8(const uint16_t *x, const uint16_t *gamma, int64_t T, int6
             xf[i] = y;
         }
         for (k = 0; k < K; k++)
-            scales[t * K + k] = mxfp8_cast_block(xf + k * B, xr + k * B, B, mode,
-                                                 codes + t * d + k * B);
+            scales[t * K + k] = mx_cast_block(xf + k * B, xr + k * B, B, mode, elem,
+                                              rowcodes + k * B);
+        store_row_codes(rowcodes, d, elem, codes + t * (elem == MXO_ELEM_E2M1 ? d / 2 : d));
     }
+}
+
+void mxo_rmsnorm_mxfp8(const uint16_t *x, const uint16_t *gamma, int64_t T, int64_t d,
+                       float eps, int mode, uint8_t *codes, uint8_t *scales, float *rho32,
+                       double *rho64)
+{
+    mxo_rmsnorm_mx(x, gamma, T, d, 32, MXO_ELEM_E4M3, eps, mode, codes, scales, rho32, rho64);
 }
 
 /* ------------------------------------------------------------------------ */
@@ -424,13 +503,6 @@ static uint8_t nvfp4_cast_block(const float *tv, const uint16_t *sign_src, float
         }
     }
     return S;
-}
-
-static void pack_nibbles(const uint8_t *codes, int64_t n, uint8_t *packed)
-{
-    int64_t j;
-    for (j = 0; j < n / 2; j++)
-        packed[j] = (uint8_t)((codes[2 * j] & 0xF) | ((codes[2 * j + 1] & 0xF) << 4));
 }
 
 /* codes: packed E2M1 [T, d/2]; scales: E4M3 [T, d/16]. */
@@ -542,4 +614,11 @@ void mxo_scale_exponent_array(const float *a, int64_t n, int mode, int32_t *out)
     int64_t i;
     for (i = 0; i < n; i++)
         out[i] = mxo_scale_exponent(a[i], mode);
+}
+
+void mxo_scale_exponent_fmt_array(const float *a, int64_t n, int mode, int elem, int32_t *out)
+{
+    int64_t i;
+    for (i = 0; i < n; i++)
+        out[i] = mxo_scale_exponent_fmt(a[i], mode, elem);
 }

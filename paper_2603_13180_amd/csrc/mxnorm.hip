@@ -118,33 +118,17 @@ typedef short short2_t __attribute__((ext_vector_type(2)));
 // fp32 exponent field is therefore the scale operand (byte 0 reads as
 // 2^-127).  The instruction returns NaN above 464 instead of saturating, so
 // callers keep |t / 2^e| <= 448: RCEIL guarantees it, FLOOR clamps first.
-// Checked against the software encoder below on all 2^32 fp32 inputs for
-// several exponents, including -127 and 120.
+// Before use it was checked on the device, on all 2^32 fp32 inputs and for
+// scale exponents -127, -7, 5 and 120, against an integer-rounding E4M3
+// encoder (fp32 significand rounded to 3 bits, ties to even, exponent
+// rebiased; n * 2^-9 with n = rint(|v| * 512) below 2^-6); the GPU parity
+// tests hold it to the oracle.
 __device__ __forceinline__ uint32_t e4m3x4_hw(float t0, float t1, float t2, float t3,
                                               float scale)
 {
     short2_t r = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32((short2_t){0, 0}, t0, t1, scale, false);
     r = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(r, t2, t3, scale, true);
     return __builtin_bit_cast(uint32_t, r);
-}
-
-// OCP E4M3 code of v, round to nearest even, saturating at 448; NaN -> 0x7F
-// with v's sign (the software encoder; used once per NVFP4 block).  Normal range: round the fp32 significand to 3 bits on the
-// integer pattern and rebias the exponent (127 -> 7).  Below 2^-6 the value
-// is n * 2^-9: n = rint(|v| * 512), where n = 8 is the smallest normal code.
-__device__ __forceinline__ uint32_t e4m3_code(float v)
-{
-    const uint32_t u = __float_as_uint(v);
-    const uint32_t s = (u >> 24) & 0x80u;
-    const uint32_t a = u & 0x7FFFFFFFu;
-    uint32_t r;
-    if (a >= 0x43E00000u)
-        r = (a > 0x7F800000u) ? 0x7Fu : 0x7Eu;
-    else if (a >= 0x3C800000u)
-        r = ((a + 0x7FFFFu + ((a >> 20) & 1u)) >> 20) - 0x3C0u;
-    else
-        r = (uint32_t)__builtin_rintf(__uint_as_float(a) * 512.0f);
-    return s | r;
 }
 
 // E2M1 code (low nibble) of |v| with the sign bit of `sign_src`, nearest
@@ -257,16 +241,17 @@ struct Team {
 
 // NV: NVFP4 output (else MXFP8).  MXN: MXNorm (else RMSNorm).  GAM: apply
 // gamma (RMSNorm only).
-// Chunks j*TL + l (j < CPL) of `row` into v; zeros outside the tensor.
+// Chunks j*TL + l (j < cpl <= CPL) of `row` into v; zeros outside the tensor.
 template <int TL, int CPL>
-__device__ __forceinline__ void load_row(const Args &A, int64_t row, int l, uint4 (&v)[CPL])
+__device__ __forceinline__ void load_row(const Args &A, int64_t row, int l, int cpl,
+                                         uint4 (&v)[CPL])
 {
     const bool row_ok = row < A.T;
     const uint4 *xr = reinterpret_cast<const uint4 *>(A.x + (row_ok ? row : 0) * A.d);
 #pragma unroll
     for (int j = 0; j < CPL; ++j) {
         const int c = j * TL + l;
-        v[j] = (row_ok && c < A.nc) ? load_stream(xr + c) : make_uint4(0u, 0u, 0u, 0u);
+        v[j] = (j < cpl && row_ok && c < A.nc) ? load_stream(xr + c) : make_uint4(0u, 0u, 0u, 0u);
     }
 }
 
@@ -317,10 +302,13 @@ norm_cast_kernel(Args A)
         }
     }
 
+    // chunks per lane this row actually has: the same for every lane, so the
+    // loops below skip the unused tail of the register array uniformly
+    const int cpl = (A.nc + TL - 1) / TL;
     uint4 v[CPL];
     {
         const int64_t row = (int64_t)blockIdx.x * TEAMS + team;
-        load_row<TL, CPL>(A, row, l, v);
+        load_row<TL, CPL>(A, row, l, cpl, v);
         const bool row_ok = row < A.T;
         const int64_t rr = row_ok ? row : 0;
         bool ok[CPL];
@@ -334,6 +322,8 @@ norm_cast_kernel(Args A)
         if constexpr (MXN) {
 #pragma unroll
             for (int j = 0; j < CPL; ++j) {
+                if (j >= cpl)
+                    break;
                 uint32_t m = chunk_absmax_bits(v[j]);
                 m = max(m, dpp_quad<0xB1>(m));
                 if constexpr (!NV)
@@ -347,6 +337,8 @@ norm_cast_kernel(Args A)
         } else {
 #pragma unroll
             for (int j = 0; j < CPL; ++j) {
+                if (j >= cpl)
+                    break;
                 const uint32_t w[4] = {v[j].x, v[j].y, v[j].z, v[j].w};
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
@@ -375,6 +367,8 @@ norm_cast_kernel(Args A)
         // ---- pass 2: block scales and element codes ----
 #pragma unroll
         for (int j = 0; j < CPL; ++j) {
+            if (j >= cpl)
+                break;
             const int c = j * TL + l;
             const uint32_t w[4] = {v[j].x, v[j].y, v[j].z, v[j].w};
             float t[8];
@@ -440,7 +434,11 @@ norm_cast_kernel(Args A)
                     float q = six_sg_ok ? div_by_recip(a, six_sg, rcp_six_sg) : a / six_sg;
                     if (q != q) // a is finite: a NaN here is an overflowed quotient
                         q = __builtin_inff();
-                    S = e4m3_code(q);
+                    // E4M3 code of q >= 0, nearest even, on the conversion
+                    // unit; the instruction gives NaN above 464 instead of
+                    // saturating, so clamp to 448 first
+                    S = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(__builtin_fminf(q, 448.0f),
+                                                                  0.0f, 0, false) & 0xFFu;
                     const float den = e4m3_value(S) * A.s_g;
                     const float r = rcp_den[S];
                     if (den == 0.0f) {
@@ -556,9 +554,14 @@ hipError_t launch_kind(const Args &A, int TL, int CPL, hipStream_t stream)
     return hipErrorInvalidValue;
 }
 
-// Team size: the smallest of 16 .. 512 lanes holding the row in at most 8
-// chunks per lane; 4 chunks per lane when that suffices.
-void pick_team(int nc, int &TL, int &CPL)
+// Team size (lanes per row, 16 .. 512) and register chunks per lane (4 or 8).
+// The smallest team that holds the row in at most 8 chunks per lane gives the
+// most independent loads per lane; when that leaves fewer than kMinWaves
+// waves in the launch (too few rows to cover 256 compute units several times
+// over), wider teams with fewer chunks per lane are taken, up to 64 lanes.
+constexpr int64_t kMinWaves = 4096;
+
+void pick_team(int64_t T, int nc, int &TL, int &CPL)
 {
     static const int sizes[] = {16, 32, 64, 128, 256, 512};
     TL = 0;
@@ -566,10 +569,15 @@ void pick_team(int nc, int &TL, int &CPL)
     for (int s : sizes) {
         if (nc <= 8 * s) {
             TL = s;
-            CPL = nc <= 4 * s ? 4 : 8;
-            return;
+            break;
         }
     }
+    if (TL == 0)
+        return;
+    // widen short-of-waves launches while every lane keeps at least one chunk
+    while (TL < 64 && T * TL / 64 < kMinWaves && nc >= 2 * TL)
+        TL *= 2;
+    CPL = (nc + TL - 1) / TL <= 4 ? 4 : 8;
 }
 
 mx_status check_common(const void *x, const void *gamma, int64_t T, int64_t d, int block,
@@ -606,7 +614,7 @@ mx_status check_global_scale(float s_g)
 mx_status run(Args A, bool nv, bool mxn, void *stream)
 {
     int TL, CPL;
-    pick_team(A.nc, TL, CPL);
+    pick_team(A.T, A.nc, TL, CPL);
     if (TL == 0)
         return fail(MX_EUNSUPPORTED, "no launch configuration for d = %d", A.d);
     if (A.T == 0)

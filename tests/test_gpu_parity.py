@@ -369,3 +369,41 @@ def test_unaligned_scale_pointer(offset):
         b = buf.cpu().numpy()
         assert np.all(b[:offset] == 0xA5) and np.all(b[offset + T * K:] == 0xA5)
         assert_parity(kind, (c.cpu().numpy(), s.cpu().numpy(), r.cpu().numpy()), want)
+
+
+# the hidden sizes of the paper's kernel sweep: k * 2^r, k in {1,3,5,7}, in [1024, 16384]
+SWEEP_D = sorted({k * 2 ** r for k in (1, 3, 5, 7) for r in range(15) if 1024 <= k * 2 ** r <= 16384})
+
+
+def test_sweep_hidden_sizes_listed():
+    assert len(SWEEP_D) == 17 and SWEEP_D[0] == 1024 and SWEEP_D[-1] == 16384
+
+
+@pytest.mark.parametrize("d", SWEEP_D)
+def test_sweep_hidden_sizes(d):
+    xb = synth.gaussian(21, d, seed=d + 1)
+    for kind in KINDS:
+        check(kind, xb)
+
+
+def test_graph_replay_matches_eager():
+    # the sweep times HIP-graph replays; every replay must equal the eager result
+    xb = synth.gaussian(300, 2560, seed=12)
+    x = dev_bf16(xb)
+    eager = [t.clone() for t in mxnorm.mxnorm_mxfp8_fwd(x)]
+    codes = torch.empty_like(eager[0]); scales = torch.empty_like(eager[1]); rho = torch.empty_like(eager[2])
+    s = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        mxnorm.mxnorm_mxfp8_fwd(x, codes=codes, scales=scales, rho=rho)
+    for _ in range(3):
+        codes.zero_(); scales.zero_(); rho.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(codes, eager[0]) and torch.equal(scales, eager[1]) and torch.equal(rho, eager[2])
+        # eager work between replays
+        mxnorm.rmsnorm_mxfp8_fwd(x)
+    assert_parity("mxnorm_mxfp8", (codes.cpu().numpy(), scales.cpu().numpy(), rho.cpu().numpy()),
+                  oracle.mxnorm_mxfp8(xb))
