@@ -40,7 +40,9 @@ def parse():
     ap.add_argument("--sweep", metavar="OUT_JSON",
                     help="instead of the headline line, run the paper's kernel sweep "
                          "(17 hidden sizes x 5 token counts) and write per-shape results")
-    ap.add_argument("--sweep-formats", default="mxfp8,nvfp4")
+    ap.add_argument("--sweep-formats",
+                    default="e4m3-b32,nvfp4,e4m3-b16,e4m3-b64,e2m1-b16,e2m1-b32,e2m1-b64",
+                    help="comma list of e4m3-b{16,32,64}, e2m1-b{16,32,64}, nvfp4")
     return ap.parse_args()
 
 
@@ -102,15 +104,7 @@ def run_sweep(path, formats):
                 xbytes = T * d * 2
                 n_sets = max(2, -(-ROTATE_MIN_BYTES // xbytes))
                 x = torch.randn(n_sets, T, d, generator=gen, device=dev).to(torch.bfloat16)
-                if fmt == "mxfp8":
-                    codes = torch.empty(n_sets, T, d, dtype=torch.uint8, device=dev)
-                    scales = torch.empty(n_sets, T, d // 32, dtype=torch.uint8, device=dev)
-                    nbytes = mxfp8_bytes(T, d)
-                    mx = lambda i: mxnorm.mxnorm_mxfp8_fwd(x[i], codes=codes[i], scales=scales[i],
-                                                          want_rho=False)
-                    rm = lambda i: mxnorm.rmsnorm_mxfp8_fwd(x[i], None, codes=codes[i],
-                                                           scales=scales[i], want_rho=False)
-                else:
+                if fmt == "nvfp4":
                     codes = torch.empty(n_sets, T, d // 2, dtype=torch.uint8, device=dev)
                     scales = torch.empty(n_sets, T, d // 16, dtype=torch.uint8, device=dev)
                     nbytes = nvfp4_bytes(T, d) - 4 * T
@@ -120,8 +114,18 @@ def run_sweep(path, formats):
                                                           want_rho=False)
                     rm = lambda i: mxnorm.rmsnorm_nvfp4_fwd(x[i], None, sr, codes=codes[i],
                                                            scales=scales[i], want_rho=False)
-                if fmt == "mxfp8":
-                    nbytes -= 4 * T
+                else:
+                    # "<elem>-b<block>": E8M0 scales per block, E4M3 or E2M1 codes
+                    elem, blk = fmt.split("-b")
+                    blk = int(blk)
+                    cw = d if elem == "e4m3" else d // 2
+                    codes = torch.empty(n_sets, T, cw, dtype=torch.uint8, device=dev)
+                    scales = torch.empty(n_sets, T, d // blk, dtype=torch.uint8, device=dev)
+                    nbytes = T * d * 2 + T * cw + T * (d // blk)
+                    mx = lambda i: mxnorm.mxnorm_mx_fwd(x[i], blk, elem, codes=codes[i],
+                                                       scales=scales[i], want_rho=False)
+                    rm = lambda i: mxnorm.rmsnorm_mx_fwd(x[i], None, blk, elem, codes=codes[i],
+                                                        scales=scales[i], want_rho=False)
                 # about 20 ms of device time per round
                 est_ms = nbytes / 5.0e12 * 1e3
                 reps = max(2, int(20.0 / max(est_ms * n_sets, 1e-3)))

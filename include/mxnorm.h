@@ -27,8 +27,9 @@
  *  - Argument errors are detected on the host and returned before any launch;
  *    nothing is written then.  mx_last_error() gives a description.
  *  - T == 0 is a valid no-op (the pointers are not used and may be NULL).
- *  - d must be a multiple of the block size (32 for MXFP8, 16 for NVFP4) and
- *    at most MXNORM_MAX_D; larger d returns MX_EUNSUPPORTED.
+ *  - d must be a multiple of the block size (32 for MXFP8, 16 for NVFP4, the
+ *    chosen block for the general MX entry points) and at most MXNORM_MAX_D;
+ *    larger d returns MX_EUNSUPPORTED.
  *
  * Semantics fixed where the paper leaves a choice (the same readings the
  * test oracle follows):
@@ -62,9 +63,17 @@ typedef enum {
 } mx_status;
 
 typedef enum {
-    MX_SCALE_RCEIL = 0,   /* e = smallest integer with amax <= 448 * 2^e */
-    MX_SCALE_FLOOR = 1    /* e = floor(log2 amax) - 8; elements saturate  */
+    MX_SCALE_RCEIL = 0,   /* e = smallest integer with amax <= max * 2^e  */
+    MX_SCALE_FLOOR = 1    /* e = floor(log2 amax) - log2(P); elements saturate */
 } mx_scale_mode;
+/* max = the element format's largest finite value (448 for E4M3, 6 for
+ * E2M1); P = its largest power of two (256 for E4M3, 4 for E2M1). */
+
+typedef enum {
+    MX_ELEM_E4M3 = 0,     /* OCP FP8 E4M3, one code per byte            */
+    MX_ELEM_E2M1 = 1      /* OCP FP4 E2M1, two codes per byte, element 2j
+                             in the low nibble of byte j                */
+} mx_elem;
 
 /*
  * MXNorm, MXFP8 output (Algorithm 2; Sec. 3.4).
@@ -111,6 +120,25 @@ mx_status mxnorm_nvfp4_fwd(const void *x, int64_t T, int64_t d, int p, float coe
 mx_status rmsnorm_nvfp4_fwd(const void *x, const void *gamma, int64_t T, int64_t d, float eps,
                             float global_scale, uint8_t *codes, uint8_t *scales, float *rho,
                             void *stream);
+
+/*
+ * MXNorm with a general MX output: `block` in {16, 32, 64} elements per E8M0
+ * scale and `elem` E4M3 or E2M1 codes (the block size and element dtype are
+ * parameters of the paper's mx_norm, and its kernel benchmark sweeps both,
+ * Sec. 4.4 and the performance appendix).  As mxnorm_mxfp8_fwd, with the
+ * scale rule of mx_scale_mode for the element format and codes [T, d]
+ * (E4M3) or [T, d/2] (E2M1); scales [T, d/block].  coef <= 0 selects the
+ * table value for (block, p).  mxnorm_mx_fwd(.., 32, MX_ELEM_E4M3, ..) is
+ * mxnorm_mxfp8_fwd.
+ */
+mx_status mxnorm_mx_fwd(const void *x, int64_t T, int64_t d, int block, int elem, int p,
+                        float coef, float eps, int scale_mode, uint8_t *codes, uint8_t *scales,
+                        float *rho, void *stream);
+
+/* RMSNorm (+ optional gain) then the general MX cast (Algorithm 1). */
+mx_status rmsnorm_mx_fwd(const void *x, const void *gamma, int64_t T, int64_t d, int block,
+                         int elem, float eps, int scale_mode, uint8_t *codes, uint8_t *scales,
+                         float *rho, void *stream);
 
 /*
  * Default NVFP4 tensor decode scales: an output bound divided by 6 * 448, so

@@ -69,12 +69,24 @@ __device__ __forceinline__ uint4 load_stream(const uint4 *p)
     return make_uint4(t.x, t.y, t.z, t.w);
 }
 
-// DPP quad permutes: lane i reads lane i^1 (0xB1 = [1,0,3,2]) or i^2
-// (0x4E = [2,3,0,1]).  Every call site runs with all lanes active.
+// Largest of v over the BL lanes (2, 4 or 8 consecutive, aligned) of a scale
+// block: quad permutes for lane i^1 and i^2, then the DPP row-half-mirror
+// (lane i <-> 7 - i inside each group of 8) to join two quads.
 template <int CTRL>
-__device__ __forceinline__ uint32_t dpp_quad(uint32_t v)
+__device__ __forceinline__ uint32_t dpp_mov(uint32_t v)
 {
     return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
+}
+
+template <int BL>
+__device__ __forceinline__ uint32_t block_max(uint32_t m)
+{
+    m = max(m, dpp_mov<0xB1>(m));
+    if constexpr (BL >= 4)
+        m = max(m, dpp_mov<0x4E>(m));
+    if constexpr (BL >= 8)
+        m = max(m, dpp_mov<0x141>(m));
+    return m;
 }
 
 typedef unsigned short ushort2_t __attribute__((ext_vector_type(2)));
@@ -95,18 +107,24 @@ __device__ __forceinline__ uint32_t chunk_absmax_bits(uint4 v)
 }
 
 // E8M0 scale byte of a block whose largest |value| is a (>= +0 or NaN): e + 127,
-// or 0xFF when a is not finite.  With E the biased fp32 exponent of a and m
-// its 23-bit significand field: RCEIL (the smallest e with a <= 448 * 2^e)
-// is e + 127 = E - 8 + [m > 0x600000], which is ((a + 0x1FFFFF) >> 23) - 8 on
-// the bit pattern; FLOOR (e = floor(log2 a) - 8) is (a >> 23) - 8.  Both are
-// clamped below at byte 0 (e = -127), which also covers zero and fp32
-// subnormals; the largest finite a gives byte 247, so no upper clamp.
+// or 0xFF when a is not finite.  With E the biased fp32 exponent of a, m its
+// 23-bit significand field, and the element format's largest finite value
+// 1.75 * 2^8 (E4M3) or 1.5 * 2^2 (E2M1): RCEIL (the smallest e with
+// a <= max * 2^e) is e + 127 = E - P + [m > 0x600000] (E4M3, P = 8) or
+// E - P + [m > 0x400000] (E2M1, P = 2), i.e. ((a + 0x1FFFFF) >> 23) - 8 and
+// ((a + 0x3FFFFF) >> 23) - 2 on the bit pattern; FLOOR (e = floor(log2 a) -
+// P, P the log2 of the format's largest power of two) is (a >> 23) - P.
+// Both are clamped below at byte 0 (e = -127), which also covers zero and
+// fp32 subnormals; the largest finite a stays below byte 254.
+template <bool FP4>
 __device__ __forceinline__ uint32_t e8m0_byte(float a, int mode)
 {
+    constexpr uint32_t P = FP4 ? 2u : 8u;
+    constexpr uint32_t ROUND = FP4 ? 0x3FFFFFu : 0x1FFFFFu;
     const uint32_t ab = __float_as_uint(a); // sign bit clear unless a is NaN
-    const uint32_t round = (mode == MX_SCALE_RCEIL) ? 0x1FFFFFu : 0u;
+    const uint32_t round = (mode == MX_SCALE_RCEIL) ? ROUND : 0u;
     const uint32_t biased = (ab + round) >> 23;
-    const uint32_t byte = max(biased, 8u) - 8u;
+    const uint32_t byte = max(biased, P) - P;
     return (ab >= 0x7F800000u) ? 0xFFu : byte;
 }
 
@@ -241,6 +259,20 @@ struct Team {
 
 // NV: NVFP4 output (else MXFP8).  MXN: MXNorm (else RMSNorm).  GAM: apply
 // gamma (RMSNorm only).
+// Output formats.  MX*: one E8M0 scale per B-element block and E4M3 (8-bit)
+// or E2M1 (4-bit, two per byte) codes; NV4: NVFP4 (16-element blocks, E4M3
+// scales times a tensor scale, E2M1 codes).
+enum OutFmt : int { MX8_B16, MX8_B32, MX8_B64, MX4_B16, MX4_B32, MX4_B64, NV4_B16 };
+
+template <int F>
+struct Fmt {
+    static constexpr int B =
+        (F == MX8_B16 || F == MX4_B16 || F == NV4_B16) ? 16 : (F == MX8_B32 || F == MX4_B32) ? 32 : 64;
+    static constexpr bool NV = F == NV4_B16;
+    static constexpr bool FP4 = F >= MX4_B16; // 4-bit codes
+    static constexpr int BL = B / 8;          // lanes (16-byte chunks) per block
+};
+
 // Chunks j*TL + l (j < cpl <= CPL) of `row` into v; zeros outside the tensor.
 template <int TL, int CPL>
 __device__ __forceinline__ void load_row(const Args &A, int64_t row, int l, int cpl,
@@ -255,18 +287,20 @@ __device__ __forceinline__ void load_row(const Args &A, int64_t row, int l, int 
     }
 }
 
-// NV: NVFP4 output (else MXFP8).  MXN: MXNorm (else RMSNorm).  GAM: apply
-// gamma (RMSNorm only).  Workgroup b handles rows b*TEAMS .. b*TEAMS+TEAMS-1,
-// one per team.  (A persistent variant that prefetches each team's next row
-// during the current one needs about twice the registers; at the resulting
-// occupancy it was slower for five of the six kernels on MI355X.)
-template <int TL, int CPL, bool NV, bool MXN, bool GAM>
+// F: output format.  MXN: MXNorm (else RMSNorm).  GAM: apply gamma (RMSNorm
+// only).  Workgroup b handles rows b*TEAMS .. b*TEAMS+TEAMS-1, one per team.
+// (A persistent variant that prefetches each team's next row during the
+// current one needs about twice the registers; at the resulting occupancy it
+// was slower for five of the six MXFP8/NVFP4 kernels on MI355X.)
+template <int TL, int CPL, int F, bool MXN, bool GAM>
 __global__ void __launch_bounds__(Team<TL>::BLOCK)
 norm_cast_kernel(Args A)
 {
     constexpr int BLOCK = Team<TL>::BLOCK;
     constexpr int TEAMS = Team<TL>::TEAMS;
-    constexpr int BL = NV ? 2 : 4; // lanes (chunks) per scale block
+    constexpr bool NV = Fmt<F>::NV;
+    constexpr bool FP4 = Fmt<F>::FP4;
+    constexpr int BL = Fmt<F>::BL; // lanes (chunks) per scale block
     __shared__ double red[TL > 64 ? BLOCK / 64 : 1];
     // the scale bytes of each row, gathered here and written with wide stores
     constexpr int KMAX = TL * CPL / BL;
@@ -324,10 +358,7 @@ norm_cast_kernel(Args A)
             for (int j = 0; j < CPL; ++j) {
                 if (j >= cpl)
                     break;
-                uint32_t m = chunk_absmax_bits(v[j]);
-                m = max(m, dpp_quad<0xB1>(m));
-                if constexpr (!NV)
-                    m = max(m, dpp_quad<0x4E>(m));
+                const uint32_t m = block_max<BL>(chunk_absmax_bits(v[j]));
                 mb[j] = m;
                 // every lane of the block adds its term: the sum is BL times
                 // the block sum, removed exactly (BL is a power of two) below
@@ -395,14 +426,11 @@ norm_cast_kernel(Args A)
 #pragma unroll
                 for (int k = 0; k < 8; ++k)
                     m = max(m, __float_as_uint(t[k]) & 0x7FFFFFFFu);
-                m = max(m, dpp_quad<0xB1>(m));
-                if constexpr (!NV)
-                    m = max(m, dpp_quad<0x4E>(m));
-                a = __uint_as_float(m);
+                a = __uint_as_float(block_max<BL>(m));
             }
 
-            if constexpr (!NV) {
-                const uint32_t byte = e8m0_byte(a, A.mode);
+            if constexpr (!NV && !FP4) {
+                const uint32_t byte = e8m0_byte<false>(a, A.mode);
                 if (A.mode == MX_SCALE_FLOOR) {
                     // |t| <= 448 * 2^e: saturate before the conversion
                     const float lim = __uint_as_float(((byte + 8u) << 23) | 0x600000u);
@@ -422,8 +450,31 @@ norm_cast_kernel(Args A)
                 if (ok[j]) {
                     *reinterpret_cast<uint2 *>(A.codes + rr * A.d + (int64_t)c * 8) =
                         make_uint2(lo, hi);
-                    if ((l & 3) == 0)
-                        sb[c >> 2] = (uint8_t)byte;
+                    if ((l % BL) == 0)
+                        sb[c / BL] = (uint8_t)byte;
+                }
+            } else if constexpr (!NV) {
+                // MXFP4: E2M1 codes of t / 2^e.  The scaled fp4 conversion
+                // divides by the scale operand's power of two, rounds to
+                // nearest even and saturates at 6 (checked on the device on all
+                // fp32 inputs for scale exponents -127 .. 120), so FLOOR needs
+                // no clamp.
+                const uint32_t byte = e8m0_byte<true>(a, A.mode);
+                const float scale = __uint_as_float(byte << 23);
+                uint32_t packed = 0;
+                packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, t[0], t[1], scale, 0);
+                packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, t[2], t[3], scale, 1);
+                packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, t[4], t[5], scale, 2);
+                packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, t[6], t[7], scale, 3);
+                if (__builtin_amdgcn_ballot_w64(byte == 0xFFu)) { // rare: non-finite input
+                    if (byte == 0xFFu)
+                        packed = 0x77777777u | sign_nibbles(v[j]);
+                }
+                if (ok[j]) {
+                    *reinterpret_cast<uint32_t *>(A.codes + rr * (A.d / 2) + (int64_t)c * 4) =
+                        packed;
+                    if ((l % BL) == 0)
+                        sb[c / BL] = (uint8_t)byte;
                 }
             } else {
                 uint32_t S, packed = 0;
@@ -526,22 +577,22 @@ float table_coef(int block, int p)
     }
 }
 
-template <int TL, int CPL, bool NV, bool MXN, bool GAM>
+template <int TL, int CPL, int F, bool MXN, bool GAM>
 hipError_t launch_one(const Args &A, hipStream_t stream)
 {
     const int64_t blocks = (A.T + Team<TL>::TEAMS - 1) / Team<TL>::TEAMS;
-    hipLaunchKernelGGL((norm_cast_kernel<TL, CPL, NV, MXN, GAM>), dim3((unsigned)blocks),
+    hipLaunchKernelGGL((norm_cast_kernel<TL, CPL, F, MXN, GAM>), dim3((unsigned)blocks),
                        dim3(Team<TL>::BLOCK), 0, stream, A);
     return hipGetLastError();
 }
 
-template <bool NV, bool MXN, bool GAM>
+template <int F, bool MXN, bool GAM>
 hipError_t launch_kind(const Args &A, int TL, int CPL, hipStream_t stream)
 {
 #define MXN_CASE(tl)                                                                     \
     case tl:                                                                             \
-        return CPL == 4 ? launch_one<tl, 4, NV, MXN, GAM>(A, stream)                     \
-                        : launch_one<tl, 8, NV, MXN, GAM>(A, stream);
+        return CPL == 4 ? launch_one<tl, 4, F, MXN, GAM>(A, stream)                      \
+                        : launch_one<tl, 8, F, MXN, GAM>(A, stream);
     switch (TL) {
         MXN_CASE(16)
         MXN_CASE(32)
@@ -552,6 +603,15 @@ hipError_t launch_kind(const Args &A, int TL, int CPL, hipStream_t stream)
     }
 #undef MXN_CASE
     return hipErrorInvalidValue;
+}
+
+template <int F>
+hipError_t launch_fmt(const Args &A, bool mxn, int TL, int CPL, hipStream_t stream)
+{
+    if (mxn)
+        return launch_kind<F, true, false>(A, TL, CPL, stream);
+    return A.gamma ? launch_kind<F, false, true>(A, TL, CPL, stream)
+                   : launch_kind<F, false, false>(A, TL, CPL, stream);
 }
 
 // Team size (lanes per row, 16 .. 512) and register chunks per lane (4 or 8).
@@ -611,7 +671,7 @@ mx_status check_global_scale(float s_g)
     return MX_OK;
 }
 
-mx_status run(Args A, bool nv, bool mxn, void *stream)
+mx_status run(Args A, int fmt, bool mxn, void *stream)
 {
     int TL, CPL;
     pick_team(A.T, A.nc, TL, CPL);
@@ -619,26 +679,39 @@ mx_status run(Args A, bool nv, bool mxn, void *stream)
         return fail(MX_EUNSUPPORTED, "no launch configuration for d = %d", A.d);
     if (A.T == 0)
         return MX_OK;
-    // widest scale store that K and the buffer's alignment allow (K <= 16*TL,
+    // widest scale store that K and the buffer's alignment allow (K <= 4*TL,
     // so 16-byte stores need at most one per lane)
     const uintptr_t sa = (uintptr_t)A.scales;
     A.sw = (A.K % 16 == 0 && sa % 16 == 0) ? 16 : (A.K % 4 == 0 && sa % 4 == 0) ? 4 : 1;
     hipStream_t st = (hipStream_t)stream;
     hipError_t e;
-    const bool gam = A.gamma != nullptr;
-    if (!nv && mxn)
-        e = launch_kind<false, true, false>(A, TL, CPL, st);
-    else if (!nv && !mxn)
-        e = gam ? launch_kind<false, false, true>(A, TL, CPL, st)
-                : launch_kind<false, false, false>(A, TL, CPL, st);
-    else if (nv && mxn)
-        e = launch_kind<true, true, false>(A, TL, CPL, st);
-    else
-        e = gam ? launch_kind<true, false, true>(A, TL, CPL, st)
-                : launch_kind<true, false, false>(A, TL, CPL, st);
+    switch (fmt) {
+    case MX8_B16: e = launch_fmt<MX8_B16>(A, mxn, TL, CPL, st); break;
+    case MX8_B32: e = launch_fmt<MX8_B32>(A, mxn, TL, CPL, st); break;
+    case MX8_B64: e = launch_fmt<MX8_B64>(A, mxn, TL, CPL, st); break;
+    case MX4_B16: e = launch_fmt<MX4_B16>(A, mxn, TL, CPL, st); break;
+    case MX4_B32: e = launch_fmt<MX4_B32>(A, mxn, TL, CPL, st); break;
+    case MX4_B64: e = launch_fmt<MX4_B64>(A, mxn, TL, CPL, st); break;
+    case NV4_B16: e = launch_fmt<NV4_B16>(A, mxn, TL, CPL, st); break;
+    default: return fail(MX_EINVAL, "unknown output format");
+    }
     if (e != hipSuccess)
         return fail(MX_EHIP, "kernel launch failed: %s", hipGetErrorString(e));
     return MX_OK;
+}
+
+// The MX format for a block size and element format, or -1.
+int mx_format(int block, int elem)
+{
+    if (elem != MX_ELEM_E4M3 && elem != MX_ELEM_E2M1)
+        return -1;
+    const int base = elem == MX_ELEM_E4M3 ? MX8_B16 : MX4_B16;
+    switch (block) {
+    case 16: return base;
+    case 32: return base + 1;
+    case 64: return base + 2;
+    default: return -1;
+    }
 }
 
 Args make_args(const void *x, const void *gamma, int64_t T, int64_t d, int block, int p,
@@ -692,7 +765,7 @@ mx_status mxnorm_mxfp8_fwd(const void *x, int64_t T, int64_t d, int p, float coe
         return fail(MX_EINVAL, "unknown scale_mode %d", scale_mode);
     return run(make_args(x, nullptr, T, d, 32, p, coef, eps, scale_mode, 1.0f, codes, scales,
                          rho),
-               false, true, stream);
+               MX8_B32, true, stream);
 }
 
 mx_status rmsnorm_mxfp8_fwd(const void *x, const void *gamma, int64_t T, int64_t d, float eps,
@@ -707,7 +780,7 @@ mx_status rmsnorm_mxfp8_fwd(const void *x, const void *gamma, int64_t T, int64_t
         return fail(MX_EINVAL, "unknown scale_mode %d", scale_mode);
     return run(make_args(x, gamma, T, d, 32, 2, 1.0f, eps, scale_mode, 1.0f, codes, scales,
                          rho),
-               false, false, stream);
+               MX8_B32, false, stream);
 }
 
 mx_status mxnorm_nvfp4_fwd(const void *x, int64_t T, int64_t d, int p, float coef, float eps,
@@ -724,7 +797,7 @@ mx_status mxnorm_nvfp4_fwd(const void *x, int64_t T, int64_t d, int p, float coe
         return st;
     return run(make_args(x, nullptr, T, d, 16, p, coef, eps, MX_SCALE_RCEIL, global_scale,
                          codes, scales, rho),
-               true, true, stream);
+               NV4_B16, true, stream);
 }
 
 mx_status rmsnorm_nvfp4_fwd(const void *x, const void *gamma, int64_t T, int64_t d, float eps,
@@ -739,7 +812,45 @@ mx_status rmsnorm_nvfp4_fwd(const void *x, const void *gamma, int64_t T, int64_t
         return st;
     return run(make_args(x, gamma, T, d, 16, 2, 1.0f, eps, MX_SCALE_RCEIL, global_scale, codes,
                          scales, rho),
-               true, false, stream);
+               NV4_B16, false, stream);
+}
+
+mx_status mxnorm_mx_fwd(const void *x, int64_t T, int64_t d, int block, int elem, int p,
+                        float coef, float eps, int scale_mode, uint8_t *codes, uint8_t *scales,
+                        float *rho, void *stream)
+{
+    g_err[0] = '\0';
+    const int fmt = mx_format(block, elem);
+    if (fmt < 0)
+        return fail(MX_EINVAL, "block must be 16, 32 or 64 and elem E4M3 or E2M1");
+    mx_status st = check_common(x, nullptr, T, d, block, eps, codes, scales, rho);
+    if (st != MX_OK)
+        return st;
+    if ((st = check_p_coef(p, coef, block)) != MX_OK)
+        return st;
+    if (scale_mode != MX_SCALE_RCEIL && scale_mode != MX_SCALE_FLOOR)
+        return fail(MX_EINVAL, "unknown scale_mode %d", scale_mode);
+    return run(make_args(x, nullptr, T, d, block, p, coef, eps, scale_mode, 1.0f, codes, scales,
+                         rho),
+               fmt, true, stream);
+}
+
+mx_status rmsnorm_mx_fwd(const void *x, const void *gamma, int64_t T, int64_t d, int block,
+                         int elem, float eps, int scale_mode, uint8_t *codes, uint8_t *scales,
+                         float *rho, void *stream)
+{
+    g_err[0] = '\0';
+    const int fmt = mx_format(block, elem);
+    if (fmt < 0)
+        return fail(MX_EINVAL, "block must be 16, 32 or 64 and elem E4M3 or E2M1");
+    mx_status st = check_common(x, gamma, T, d, block, eps, codes, scales, rho);
+    if (st != MX_OK)
+        return st;
+    if (scale_mode != MX_SCALE_RCEIL && scale_mode != MX_SCALE_FLOOR)
+        return fail(MX_EINVAL, "unknown scale_mode %d", scale_mode);
+    return run(make_args(x, gamma, T, d, block, 2, 1.0f, eps, scale_mode, 1.0f, codes, scales,
+                         rho),
+               fmt, false, stream);
 }
 
 float mxnorm_default_global_scale(int64_t d, int block, int p, float coef)

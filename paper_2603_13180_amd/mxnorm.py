@@ -16,6 +16,7 @@ LIB_PATH = os.path.join(_HERE, "libmxnorm.so")
 
 MX_OK, MX_EINVAL, MX_EUNSUPPORTED, MX_EHIP = 0, 1, 2, 3
 SCALE_MODES = {"rceil": 0, "floor": 1}
+ELEMS = {"e4m3": 0, "e2m1": 1}
 ABI_VERSION = 1
 MAX_D = 32768
 
@@ -47,6 +48,8 @@ def load():
         "rmsnorm_mxfp8_fwd": (I, [P, P, I64, I64, F, I, P, P, P, P]),
         "mxnorm_nvfp4_fwd": (I, [P, I64, I64, I, F, F, F, P, P, P, P]),
         "rmsnorm_nvfp4_fwd": (I, [P, P, I64, I64, F, F, P, P, P, P]),
+        "mxnorm_mx_fwd": (I, [P, I64, I64, I, I, I, F, F, I, P, P, P, P]),
+        "rmsnorm_mx_fwd": (I, [P, P, I64, I64, I, I, F, I, P, P, P, P]),
         "mxnorm_default_global_scale": (F, [I64, I, I, F]),
         "rmsnorm_default_global_scale": (F, [I64, F]),
         "mxnorm_coef": (F, [I, I]),
@@ -170,6 +173,44 @@ def rmsnorm_nvfp4_fwd(x, gamma=None, global_scale=None, eps=1e-6,
     _check(load().rmsnorm_nvfp4_fwd(_ptr(x), _ptr(g), T, d, eps, global_scale, _ptr(codes),
                                     _ptr(scales), _ptr(rho) if want_rho else None,
                                     _stream(x.device)))
+    return codes, scales, (rho if want_rho else None)
+
+
+def _mx_out_shapes(T, d, block, elem):
+    if block not in (16, 32, 64) or elem not in ELEMS:
+        raise ValueError("block must be 16, 32 or 64 and elem 'e4m3' or 'e2m1'")
+    return ((T, d) if elem == "e4m3" else (T, d // 2)), (T, d // block)
+
+
+def mxnorm_mx_fwd(x, block=32, elem="e4m3", p=2, coef=0.0, eps=1e-6, scale_mode="rceil",
+                  codes=None, scales=None, rho=None, want_rho=True):
+    """MXNorm with a general MX output: E8M0 scales per `block` elements and
+    E4M3 or E2M1 (packed two per byte) codes."""
+    T, d = _input(x)
+    cs, ss = _mx_out_shapes(T, d, block, elem)
+    codes = _out(codes, cs, torch.uint8, x.device)
+    scales = _out(scales, ss, torch.uint8, x.device)
+    if want_rho:
+        rho = _out(rho, (T,), torch.float32, x.device)
+    _check(load().mxnorm_mx_fwd(_ptr(x), T, d, block, ELEMS[elem], p, coef, eps,
+                                SCALE_MODES[scale_mode], _ptr(codes), _ptr(scales),
+                                _ptr(rho) if want_rho else None, _stream(x.device)))
+    return codes, scales, (rho if want_rho else None)
+
+
+def rmsnorm_mx_fwd(x, gamma=None, block=32, elem="e4m3", eps=1e-6, scale_mode="rceil",
+                   codes=None, scales=None, rho=None, want_rho=True):
+    """RMSNorm (+ optional gain) then the general MX cast."""
+    T, d = _input(x)
+    g = _gamma(gamma, x)
+    cs, ss = _mx_out_shapes(T, d, block, elem)
+    codes = _out(codes, cs, torch.uint8, x.device)
+    scales = _out(scales, ss, torch.uint8, x.device)
+    if want_rho:
+        rho = _out(rho, (T,), torch.float32, x.device)
+    _check(load().rmsnorm_mx_fwd(_ptr(x), _ptr(g), T, d, block, ELEMS[elem], eps,
+                                 SCALE_MODES[scale_mode], _ptr(codes), _ptr(scales),
+                                 _ptr(rho) if want_rho else None, _stream(x.device)))
     return codes, scales, (rho if want_rho else None)
 
 

@@ -150,3 +150,21 @@ def test_binding_refuses_cpu_tensors():
         mxnorm.mxnorm_mxfp8_fwd(x)
     with pytest.raises(TypeError):
         mxnorm.mxnorm_mxfp8_fwd(torch.zeros(4, 64))
+
+
+@pytest.mark.parametrize("args,status", [
+    ((A16, 4, 64, 8, 0), 1),     # block 8
+    ((A16, 4, 64, 128, 0), 1),   # block 128
+    ((A16, 4, 64, 32, 2), 1),    # element format
+    ((A16, 4, 48, 32, 0), 1),    # d % block
+    ((A16, 4, 96, 64, 1), 1),    # d % 64
+    ((A16, 4, 65536, 64, 0), 2), # d too large
+    ((None, 0, 64, 64, 1), 0),   # T = 0
+])
+def test_generic_mx_entry_points_validate(args, status):
+    lib = mxnorm.load()
+    x, T, d, block, elem = args
+    assert lib.mxnorm_mx_fwd(x, T, d, block, elem, 2, 0.0, 1e-6, 0, OUT if T else None,
+                             OUT if T else None, None, None) == status
+    assert lib.rmsnorm_mx_fwd(x, None, T, d, block, elem, 1e-6, 0, OUT if T else None,
+                              OUT if T else None, None, None) == status

@@ -407,3 +407,64 @@ def test_graph_replay_matches_eager():
         mxnorm.rmsnorm_mxfp8_fwd(x)
     assert_parity("mxnorm_mxfp8", (codes.cpu().numpy(), scales.cpu().numpy(), rho.cpu().numpy()),
                   oracle.mxnorm_mxfp8(xb))
+
+
+
+# ----------------------------------------------------- general MX formats --
+
+MX_FORMATS = [(16, "e4m3"), (32, "e4m3"), (64, "e4m3"), (16, "e2m1"), (32, "e2m1"), (64, "e2m1")]
+
+
+def check_mx(xb, block, elem, gb=None, mxn=True, **kw):
+    x = dev_bf16(xb)
+    if mxn:
+        got = mxnorm.mxnorm_mx_fwd(x, block=block, elem=elem, **kw)
+        c = kw.pop("coef", 0.0)
+        want = oracle.mxnorm_mx(xb, B=block, elem=elem, coef_=None if c <= 0 else c,
+                                p=kw.get("p", 2), eps=kw.get("eps", 1e-6),
+                                mode=kw.get("scale_mode", "rceil"))
+    else:
+        g = None if gb is None else dev_bf16(gb)
+        got = mxnorm.rmsnorm_mx_fwd(x, g, block=block, elem=elem, **kw)
+        want = oracle.rmsnorm_mx(xb, gb, B=block, elem=elem, eps=kw.get("eps", 1e-6),
+                                 mode=kw.get("scale_mode", "rceil"))
+    torch.cuda.synchronize()
+    assert_parity("mx B=%d %s %s" % (block, elem, "mxnorm" if mxn else "rmsnorm"),
+                  tuple(t.cpu().numpy() for t in got), want, "shape=%s %s" % (xb.shape, kw))
+
+
+@pytest.mark.parametrize("block,elem", MX_FORMATS)
+@pytest.mark.parametrize("T,d", [(3, 64), (65, 192), (130, 1024), (33, 1280), (257, 4096),
+                                 (9, 10240), (4, 32768)])
+def test_mx_formats_shapes(block, elem, T, d):
+    xb = synth.gaussian(T, d, seed=T + d + block, scale=2.0)
+    gb = synth.f32_to_bf16_bits(np.random.default_rng(d).uniform(0.5, 1.5, d).astype(np.float32))
+    check_mx(xb, block, elem)
+    check_mx(xb, block, elem, gb, mxn=False)
+    check_mx(xb, block, elem, None, mxn=False)
+
+
+@pytest.mark.parametrize("block,elem", MX_FORMATS)
+def test_mx_formats_modes_p_eps_and_edge_rows(block, elem):
+    xb = synth.gaussian(100, 2048, seed=block, scale=0.5)
+    for p in (1, 2):
+        for eps in (0.0, 1e-6):
+            check_mx(xb, block, elem, p=p, eps=eps)
+            check_mx(xb, block, elem, p=p, eps=eps, scale_mode="floor")
+    check_mx(xb, block, elem, coef=0.77)
+    for d in (64, 1024):
+        ab = adversarial_rows(d, seed=block + d)
+        for mode in ("rceil", "floor"):
+            for eps in (0.0, 1e-6):
+                check_mx(ab, block, elem, eps=eps, scale_mode=mode)
+                check_mx(ab, block, elem, None, mxn=False, eps=eps, scale_mode=mode)
+
+
+def test_mx_b32_e4m3_equals_mxfp8_entry_point():
+    xb = synth.gaussian(77, 4096, seed=3)
+    x = dev_bf16(xb)
+    a = mxnorm.mxnorm_mx_fwd(x, block=32, elem="e4m3")
+    b = mxnorm.mxnorm_mxfp8_fwd(x)
+    torch.cuda.synchronize()
+    for u, v in zip(a, b):
+        assert torch.equal(u, v)
