@@ -305,15 +305,17 @@ norm_cast_kernel(Args A)
     // the scale bytes of each row, gathered here and written with wide stores
     constexpr int KMAX = TL * CPL / BL;
     __shared__ __attribute__((aligned(16))) uint8_t sbuf[TEAMS * KMAX];
-    // NVFP4: 1 / RN(dec(S) s_g) for every finite E4M3 block scale S, one IEEE
-    // division per entry per workgroup instead of one per block
-    __shared__ float rcp_den[NV ? 128 : 1];
+    // NVFP4: for every finite E4M3 block scale S, den = RN(dec(S) s_g) and
+    // its correctly rounded reciprocal -- one IEEE division per entry per
+    // workgroup instead of one per block.  A zero reciprocal marks the scales
+    // whose blocks take the exact slow path (den = 0 or den < 2^-90).
+    __shared__ float2 den_tab[NV ? 128 : 1];
     float six_sg = 0.0f, rcp_six_sg = 0.0f;
     bool six_sg_ok = false;
     if constexpr (NV) {
         if (threadIdx.x < 127) {
             const float den = e4m3_value(threadIdx.x) * A.s_g;
-            rcp_den[threadIdx.x] = 1.0f / den;
+            den_tab[threadIdx.x] = make_float2(den, den >= 0x1p-90f ? 1.0f / den : 0.0f);
         }
         six_sg = 6.0f * A.s_g;
         rcp_six_sg = 1.0f / six_sg;
@@ -490,13 +492,9 @@ norm_cast_kernel(Args A)
                     // saturating, so clamp to 448 first
                     S = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(__builtin_fminf(q, 448.0f),
                                                                   0.0f, 0, false) & 0xFFu;
-                    const float den = e4m3_value(S) * A.s_g;
-                    const float r = rcp_den[S];
-                    if (den == 0.0f) {
-#pragma unroll
-                        for (int k = 0; k < 8; ++k)
-                            packed |= ((__float_as_uint(t[k]) >> 31) << 3) << (4 * k);
-                    } else if (den >= 0x1p-90f && a * r <= 0x1p100f) {
+                    const float2 dr = den_tab[S];
+                    const float den = dr.x, r = dr.y;
+                    if (r > 0.0f && a * r <= 0x1p100f) {
                         // common case: every quotient is finite and the
                         // Markstein correction is exact; the sign is taken
                         // from t so zero and underflowing quotients keep it
@@ -508,6 +506,10 @@ norm_cast_kernel(Args A)
                         packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, vq[2], vq[3], 1.0f, 1);
                         packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, vq[4], vq[5], 1.0f, 2);
                         packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, vq[6], vq[7], 1.0f, 3);
+                    } else if (den == 0.0f) {
+#pragma unroll
+                        for (int k = 0; k < 8; ++k)
+                            packed |= ((__float_as_uint(t[k]) >> 31) << 3) << (4 * k);
                     } else {
 #pragma unroll
                         for (int k = 0; k < 8; ++k)
