@@ -76,6 +76,8 @@ def _load():
         "mxo_mxcast": (None, [P, I64, I64, I, I, I, P, P]),
         "mxo_mxnorm_mx": (None, [P, I64, I64, I, I, I, F, F, I, P, P, P, P]),
         "mxo_rmsnorm_mx": (None, [P, P, I64, I64, I, I, F, I, P, P, P, P]),
+        "mxo_mxcast_gain": (None, [P, P, I64, I64, I, I, I, P, P]),
+        "mxo_mx_matmul": (None, [P, P, P, P, I64, I64, I64, I, I, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -298,3 +300,41 @@ def rmsnorm_mx(x, gamma=None, B=32, elem="e4m3", eps=1e-6, mode="rceil"):
     _load().mxo_rmsnorm_mx(_ptr(x), _ptr(g), T, d, B, ELEMS[elem], eps, SCALE_MODES[mode],
                            _ptr(codes), _ptr(scales), _ptr(r32), _ptr(r64))
     return codes, scales, r32, r64
+
+
+# ----------------------------------------------------------- MXNormLinear --
+
+def mxcast_gain(w, gamma=None, B=32, elem="e4m3", mode="rceil"):
+    """MXCast(W gamma) of the implementation appendix's mx_norm_linear_forward:
+    w bf16 bits [N, d], gamma bf16 bits [d] or None; the product in float."""
+    w = _as_bf16_rows(w)
+    N, d = w.shape
+    cshape, sshape = _mx_shapes(N, d, B, elem)
+    g = _as_gamma(gamma, d)
+    codes = np.empty(cshape, np.uint8)
+    scales = np.empty(sshape, np.uint8)
+    _load().mxo_mxcast_gain(_ptr(w), _ptr(g), N, d, B, ELEMS[elem], SCALE_MODES[mode],
+                            _ptr(codes), _ptr(scales))
+    return codes, scales
+
+
+def mx_matmul(a_codes, a_scales, b_codes, b_scales, K, B=32, elem="e4m3"):
+    """H = dec(A) dec(B)^T in double (eq. mx-matmul), A [M, K], B [N, K]."""
+    a_codes = np.ascontiguousarray(a_codes, np.uint8)
+    b_codes = np.ascontiguousarray(b_codes, np.uint8)
+    a_scales = np.ascontiguousarray(a_scales, np.uint8)
+    b_scales = np.ascontiguousarray(b_scales, np.uint8)
+    M, N = a_codes.shape[0], b_codes.shape[0]
+    h = np.empty((M, N), np.float64)
+    _load().mxo_mx_matmul(_ptr(a_codes), _ptr(a_scales), _ptr(b_codes), _ptr(b_scales), M, N, K,
+                          B, ELEMS[elem], _ptr(h))
+    return h
+
+
+def mxnorm_linear(x, w, gamma=None, B=32, elem="e4m3", p=2, eps=1e-6, mode="rceil"):
+    """The MXNormLinear forward, H = MXNorm(X) MXCast(W gamma)^T (Sec. 3.7),
+    composed from the three oracle steps.  Returns (H, activation codes,
+    activation scales, rho32)."""
+    ac, as_, r32, _ = mxnorm_mx(x, B=B, elem=elem, p=p, eps=eps, mode=mode)
+    wc, ws = mxcast_gain(w, gamma, B=B, elem=elem, mode=mode)
+    return mx_matmul(ac, as_, wc, ws, x.shape[1], B=B, elem=elem), ac, as_, r32

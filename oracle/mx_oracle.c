@@ -622,3 +622,63 @@ void mxo_scale_exponent_fmt_array(const float *a, int64_t n, int mode, int elem,
     for (i = 0; i < n; i++)
         out[i] = mxo_scale_exponent_fmt(a[i], mode, elem);
 }
+
+/* ------------------------------------------------------------------------ */
+/* MXNormLinear forward (Sec. 3.7 eq. (mx-matmul); the implementation         */
+/* appendix's mx_norm_linear_forward)                                        */
+/* ------------------------------------------------------------------------ */
+
+/* MXCast(W gamma): the gain folded into the next layer's weight, w' = RN32(w
+ * gamma) per column (gamma indexes the input dimension d), then the plain MX
+ * cast along d.  w: bf16 bits [N, d]; gamma: bf16 bits [d] or NULL. */
+void mxo_mxcast_gain(const uint16_t *w, const uint16_t *gamma, int64_t N, int64_t d, int B,
+                     int elem, int mode, uint8_t *codes, uint8_t *scales)
+{
+    int64_t n, i, k, K = d / B;
+    float y[65536];
+    uint8_t rowcodes[65536];
+    for (n = 0; n < N; n++) {
+        for (i = 0; i < d; i++) {
+            y[i] = mxo_bf16_to_float(w[n * d + i]);
+            if (gamma)
+                y[i] = y[i] * mxo_bf16_to_float(gamma[i]);
+        }
+        for (k = 0; k < K; k++)
+            scales[n * K + k] = mx_cast_block(y + k * B, NULL, B, mode, elem, rowcodes + k * B);
+        store_row_codes(rowcodes, d, elem, codes + n * (elem == MXO_ELEM_E2M1 ? d / 2 : d));
+    }
+}
+
+/* Value of element i of an MX row: code value times its block's E8M0 scale. */
+static double mx_element(const uint8_t *codes_row, const uint8_t *scales_row, int64_t i, int B,
+                         int elem)
+{
+    double v;
+    if (elem == MXO_ELEM_E2M1) {
+        uint8_t byte = codes_row[i / 2];
+        v = mxo_e2m1_value((i & 1) ? (uint8_t)(byte >> 4) : (uint8_t)(byte & 0xF));
+    } else {
+        v = mxo_e4m3_value(codes_row[i]);
+    }
+    return v * mxo_e8m0_value(scales_row[i / B]);
+}
+
+/* H = A B^T for MX matrices A [M, K] and B [N, K] (both blocked along K):
+ * H[m][n] = sum_k dec(A)[m][k] dec(B)[n][k], the matmul of eq. (mx-matmul)
+ * "accumulated in higher precision" -- here in double, in index order. */
+void mxo_mx_matmul(const uint8_t *a_codes, const uint8_t *a_scales, const uint8_t *b_codes,
+                   const uint8_t *b_scales, int64_t M, int64_t N, int64_t K, int B, int elem,
+                   double *h)
+{
+    const int64_t cw = elem == MXO_ELEM_E2M1 ? K / 2 : K, sw = K / B;
+    int64_t m, n, k;
+    for (m = 0; m < M; m++) {
+        for (n = 0; n < N; n++) {
+            double s = 0.0;
+            for (k = 0; k < K; k++)
+                s += mx_element(a_codes + m * cw, a_scales + m * sw, k, B, elem) *
+                     mx_element(b_codes + n * cw, b_scales + n * sw, k, B, elem);
+            h[m * N + n] = s;
+        }
+    }
+}
