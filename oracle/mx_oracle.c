@@ -630,7 +630,8 @@ void mxo_scale_exponent_fmt_array(const float *a, int64_t n, int mode, int elem,
 
 /* MXCast(W gamma): the gain folded into the next layer's weight, w' = RN32(w
  * gamma) per column (gamma indexes the input dimension d), then the plain MX
- * cast along d.  w: bf16 bits [N, d]; gamma: bf16 bits [d] or NULL. */
+ * cast along d; a NaN block takes its codes' signs from w (R8).  w: bf16 bits
+ * [N, d]; gamma: bf16 bits [d] or NULL. */
 void mxo_mxcast_gain(const uint16_t *w, const uint16_t *gamma, int64_t N, int64_t d, int B,
                      int elem, int mode, uint8_t *codes, uint8_t *scales)
 {
@@ -644,7 +645,8 @@ void mxo_mxcast_gain(const uint16_t *w, const uint16_t *gamma, int64_t N, int64_
                 y[i] = y[i] * mxo_bf16_to_float(gamma[i]);
         }
         for (k = 0; k < K; k++)
-            scales[n * K + k] = mx_cast_block(y + k * B, NULL, B, mode, elem, rowcodes + k * B);
+            scales[n * K + k] = mx_cast_block(y + k * B, w + n * d + k * B, B, mode, elem,
+                                              rowcodes + k * B);
         store_row_codes(rowcodes, d, elem, codes + n * (elem == MXO_ELEM_E2M1 ? d / 2 : d));
     }
 }
