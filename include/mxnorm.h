@@ -141,6 +141,18 @@ mx_status rmsnorm_mx_fwd(const void *x, const void *gamma, int64_t T, int64_t d,
                          float *rho, void *stream);
 
 /*
+ * The plain MX cast of x, or of x * gamma (gamma NULL or bf16 [d]), with no
+ * normalisation: y = RN(x * gamma), then E8M0 scales per `block` elements
+ * and E4M3 or E2M1 codes exactly as in the entry points above.  With x = a
+ * linear layer's weight W [N, d] (rows = output features) and gamma the norm
+ * gain, this is MXCast(W gamma), the gain folded into the next weight that
+ * the MXNormLinear forward multiplies MXNorm(X) with (Sec. 3.7 eq.
+ * (mx-matmul); the implementation appendix's mx_norm_linear_forward).
+ */
+mx_status mx_cast_fwd(const void *x, const void *gamma, int64_t T, int64_t d, int block,
+                      int elem, int scale_mode, uint8_t *codes, uint8_t *scales, void *stream);
+
+/*
  * Default NVFP4 tensor decode scales: an output bound divided by 6 * 448, so
  * the bound maps to the largest E2M1 x E4M3 magnitude.  MXNorm: Lemma 2's
  * bound K^(1/p) / coef (K = d / block; coef <= 0 selects the table value);

@@ -31,526 +31,37 @@
 #include <stdio.h>
 
 #include "mxnorm.h"
+#include "norm_cast.h"
 
-#pragma clang fp contract(off)
+namespace mxk {
+
+hipError_t launch_norm_cast_MX8_B16(const Args &A, int kind, int TL, int CPL, hipStream_t stream);
+hipError_t launch_norm_cast_MX8_B32(const Args &A, int kind, int TL, int CPL, hipStream_t stream);
+hipError_t launch_norm_cast_MX8_B64(const Args &A, int kind, int TL, int CPL, hipStream_t stream);
+hipError_t launch_norm_cast_MX4_B16(const Args &A, int kind, int TL, int CPL, hipStream_t stream);
+hipError_t launch_norm_cast_MX4_B32(const Args &A, int kind, int TL, int CPL, hipStream_t stream);
+hipError_t launch_norm_cast_MX4_B64(const Args &A, int kind, int TL, int CPL, hipStream_t stream);
+hipError_t launch_norm_cast_NV4_B16(const Args &A, int kind, int TL, int CPL, hipStream_t stream);
+
+hipError_t launch_norm_cast(int fmt, const Args &A, int kind, int TL, int CPL, hipStream_t stream)
+{
+    switch (fmt) {
+    case MX8_B16: return launch_norm_cast_MX8_B16(A, kind, TL, CPL, stream);
+    case MX8_B32: return launch_norm_cast_MX8_B32(A, kind, TL, CPL, stream);
+    case MX8_B64: return launch_norm_cast_MX8_B64(A, kind, TL, CPL, stream);
+    case MX4_B16: return launch_norm_cast_MX4_B16(A, kind, TL, CPL, stream);
+    case MX4_B32: return launch_norm_cast_MX4_B32(A, kind, TL, CPL, stream);
+    case MX4_B64: return launch_norm_cast_MX4_B64(A, kind, TL, CPL, stream);
+    case NV4_B16: return launch_norm_cast_NV4_B16(A, kind, TL, CPL, stream);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+} // namespace mxk
 
 namespace {
 
-struct Args {
-    const uint16_t *x;
-    const uint16_t *gamma;
-    uint8_t *codes;
-    uint8_t *scales;
-    float *rho;
-    int64_t T;
-    int d;      // hidden size
-    int nc;     // 16-byte chunks per row (d / 8)
-    int K;      // scale blocks per row
-    int p;      // p-mean exponent (1 or 2)
-    float coef; // RMS / G_p ratio
-    float eps;
-    int mode;   // MX_SCALE_RCEIL or MX_SCALE_FLOOR
-    float s_g;  // NVFP4 tensor decode scale
-    int sw;     // bytes per scale store: 16, 4 or 1 (set from K and alignment)
-};
-
-// ---------------------------------------------------------------- helpers --
-
-__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
-__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
-
-typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
-
-// Streaming 16-byte load: each input byte is read exactly once, so mark it
-// non-temporal.
-__device__ __forceinline__ uint4 load_stream(const uint4 *p)
-{
-    const u32x4_t t = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(p));
-    return make_uint4(t.x, t.y, t.z, t.w);
-}
-
-// Largest of v over the BL lanes (2, 4 or 8 consecutive, aligned) of a scale
-// block: quad permutes for lane i^1 and i^2, then the DPP row-half-mirror
-// (lane i <-> 7 - i inside each group of 8) to join two quads.
-template <int CTRL>
-__device__ __forceinline__ uint32_t dpp_mov(uint32_t v)
-{
-    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
-}
-
-template <int BL>
-__device__ __forceinline__ uint32_t block_max(uint32_t m)
-{
-    m = max(m, dpp_mov<0xB1>(m));
-    if constexpr (BL >= 4)
-        m = max(m, dpp_mov<0x4E>(m));
-    if constexpr (BL >= 8)
-        m = max(m, dpp_mov<0x141>(m));
-    return m;
-}
-
-typedef unsigned short ushort2_t __attribute__((ext_vector_type(2)));
-
-// Largest |x| of 8 bf16 values as the 15-bit magnitude pattern.  Unsigned
-// order of bf16 magnitudes is numeric order, with NaN above Inf, so a NaN
-// input propagates.
-__device__ __forceinline__ uint32_t chunk_absmax_bits(uint4 v)
-{
-    const uint32_t m = 0x7FFF7FFFu;
-    ushort2_t a = __builtin_bit_cast(ushort2_t, v.x & m);
-    ushort2_t b = __builtin_bit_cast(ushort2_t, v.y & m);
-    ushort2_t c = __builtin_bit_cast(ushort2_t, v.z & m);
-    ushort2_t d = __builtin_bit_cast(ushort2_t, v.w & m);
-    ushort2_t r = __builtin_elementwise_max(__builtin_elementwise_max(a, b),
-                                            __builtin_elementwise_max(c, d));
-    return r.x > r.y ? (uint32_t)r.x : (uint32_t)r.y;
-}
-
-// E8M0 scale byte of a block whose largest |value| is a (>= +0 or NaN): e + 127,
-// or 0xFF when a is not finite.  With E the biased fp32 exponent of a, m its
-// 23-bit significand field, and the element format's largest finite value
-// 1.75 * 2^8 (E4M3) or 1.5 * 2^2 (E2M1): RCEIL (the smallest e with
-// a <= max * 2^e) is e + 127 = E - P + [m > 0x600000] (E4M3, P = 8) or
-// E - P + [m > 0x400000] (E2M1, P = 2), i.e. ((a + 0x1FFFFF) >> 23) - 8 and
-// ((a + 0x3FFFFF) >> 23) - 2 on the bit pattern; FLOOR (e = floor(log2 a) -
-// P, P the log2 of the format's largest power of two) is (a >> 23) - P.
-// Both are clamped below at byte 0 (e = -127), which also covers zero and
-// fp32 subnormals; the largest finite a stays below byte 254.
-template <bool FP4>
-__device__ __forceinline__ uint32_t e8m0_byte(float a, int mode)
-{
-    constexpr uint32_t P = FP4 ? 2u : 8u;
-    constexpr uint32_t ROUND = FP4 ? 0x3FFFFFu : 0x1FFFFFu;
-    const uint32_t ab = __float_as_uint(a); // sign bit clear unless a is NaN
-    const uint32_t round = (mode == MX_SCALE_RCEIL) ? ROUND : 0u;
-    const uint32_t biased = (ab + round) >> 23;
-    const uint32_t byte = max(biased, P) - P;
-    return (ab >= 0x7F800000u) ? 0xFFu : byte;
-}
-
-typedef short short2_t __attribute__((ext_vector_type(2)));
-
-// Four E4M3 codes (one dword, element 0 in the low byte) of t0..t3 / 2^e.
-// v_cvt_scalef32_pk_fp8_f32 divides by 2^(exponent field of the scale
-// operand - 127) and rounds to nearest even; the E8M0 byte shifted into the
-// fp32 exponent field is therefore the scale operand (byte 0 reads as
-// 2^-127).  The instruction returns NaN above 464 instead of saturating, so
-// callers keep |t / 2^e| <= 448: RCEIL guarantees it, FLOOR clamps first.
-// Before use it was checked on the device, on all 2^32 fp32 inputs and for
-// scale exponents -127, -7, 5 and 120, against an integer-rounding E4M3
-// encoder (fp32 significand rounded to 3 bits, ties to even, exponent
-// rebiased; n * 2^-9 with n = rint(|v| * 512) below 2^-6); the GPU parity
-// tests hold it to the oracle.
-__device__ __forceinline__ uint32_t e4m3x4_hw(float t0, float t1, float t2, float t3,
-                                              float scale)
-{
-    short2_t r = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32((short2_t){0, 0}, t0, t1, scale, false);
-    r = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(r, t2, t3, scale, true);
-    return __builtin_bit_cast(uint32_t, r);
-}
-
-// E2M1 code (low nibble) of |v| with the sign bit of `sign_src`, nearest
-// even, saturating at 6 (a NaN magnitude, which only an overflowed quotient
-// produces here, saturates too).  [1, 6): round the significand to 1 bit and
-// rebias (127 -> 1); below 1 the value is n * 0.5 with n = rint(2 |v|).
-__device__ __forceinline__ uint32_t e2m1_code(float v, float sign_src)
-{
-    const uint32_t s = (__float_as_uint(sign_src) >> 28) & 0x8u;
-    const uint32_t a = __float_as_uint(v) & 0x7FFFFFFFu;
-    uint32_t r;
-    if (a >= 0x40C00000u)
-        r = 7u;
-    else if (a >= 0x3F800000u)
-        r = ((a + 0x1FFFFFu + ((a >> 22) & 1u)) >> 22) - 0xFCu;
-    else
-        r = (uint32_t)__builtin_rintf(__uint_as_float(a) * 2.0f);
-    return s | r;
-}
-
-// Value of a non-negative finite E4M3 code.
-__device__ __forceinline__ float e4m3_value(uint32_t S)
-{
-    const uint32_t E = S >> 3, M = S & 7u;
-    return E ? __uint_as_float(((E + 120u) << 23) | (M << 20)) : (float)M * 0x1p-9f;
-}
-
-// Correctly rounded t / den from the correctly rounded reciprocal r = 1/den:
-// one product and one fused correction (Markstein).  Exact for den >= 2^-90
-// whenever |t / den| >= 2^-20; smaller quotients are below every E2M1 and
-// E4M3 rounding threshold, so the code is unaffected.
-__device__ __forceinline__ float div_by_recip(float t, float den, float r)
-{
-    const float q0 = t * r;
-    const float rem = __builtin_fmaf(-q0, den, t);
-    return __builtin_fmaf(rem, r, q0);
-}
-
-// Codes of a NaN block: each element's bf16 sign bit with an all-ones
-// magnitude.  w0, w1 hold four bf16 values (elements 0..3).
-__device__ __forceinline__ uint32_t nan_codes_e4m3(uint32_t w0, uint32_t w1)
-{
-    return 0x7F7F7F7Fu | ((w0 >> 8) & 0x80u) | ((w0 >> 16) & 0x8000u) |
-           ((w1 << 8) & 0x800000u) | (w1 & 0x80000000u);
-}
-
-__device__ __forceinline__ uint32_t sign_nibbles(uint4 v)
-{
-    // bit 15 of bf16 element k -> bit 4k+3
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-    uint32_t r = 0;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        r |= ((w[i] >> 15) & 1u) << (8 * i + 3);
-        r |= ((w[i] >> 31) & 1u) << (8 * i + 7);
-    }
-    return r;
-}
-
-// rho~ = (r^2 + eps)^(-1/2), r = coef * G_p, G_p from the sum S of m~^p over
-// K blocks (Alg. 2; Sec. 3.4).  Double precision, rounded once to float.
-__device__ __forceinline__ float rho_estimate(double S, int K, int p, float coef, float eps)
-{
-    const double G = (p == 1) ? S / (double)K : sqrt(S / (double)K);
-    const double r = (double)coef * G;
-    const double u = r * r + (double)eps;
-    return (u == 0.0) ? 0.0f : (float)(1.0 / sqrt(u));
-}
-
-// rho = ((1/d) sum x^2 + eps)^(-1/2) (Sec. 3.1 eq. (rms)).
-__device__ __forceinline__ float rho_rms(double S, int d, float eps)
-{
-    const double u = S / (double)d + (double)eps;
-    return (u == 0.0) ? 0.0f : (float)(1.0 / sqrt(u));
-}
-
-// Sum of one double per lane over a team of TL lanes.  Butterfly inside the
-// wave (every lane ends with the same bits: each step adds the same two
-// values), then, for multi-wave teams, per-wave partials through LDS.
-template <int TL>
-__device__ __forceinline__ double team_sum(double s, double *red, int tid)
-{
-    constexpr int W = TL < 64 ? TL : 64;
-#pragma unroll
-    for (int off = 1; off < W; off <<= 1)
-        s += __shfl_xor(s, off, W);
-    if constexpr (TL > 64) {
-        constexpr int NW = TL / 64;
-        const int wave = tid >> 6;
-        if ((tid & 63) == 0)
-            red[wave] = s;
-        __syncthreads();
-        const int first = (wave / NW) * NW;
-        double t = 0.0;
-#pragma unroll
-        for (int i = 0; i < NW; ++i)
-            t += red[first + i];
-        s = t;
-    }
-    return s;
-}
-
-// ------------------------------------------------------------------ kernel --
-
-template <int TL>
-struct Team {
-    static constexpr int BLOCK = TL > 256 ? TL : 256;
-    static constexpr int TEAMS = BLOCK / TL; // rows per workgroup
-};
-
-// NV: NVFP4 output (else MXFP8).  MXN: MXNorm (else RMSNorm).  GAM: apply
-// gamma (RMSNorm only).
-// Output formats.  MX*: one E8M0 scale per B-element block and E4M3 (8-bit)
-// or E2M1 (4-bit, two per byte) codes; NV4: NVFP4 (16-element blocks, E4M3
-// scales times a tensor scale, E2M1 codes).
-enum OutFmt : int { MX8_B16, MX8_B32, MX8_B64, MX4_B16, MX4_B32, MX4_B64, NV4_B16 };
-
-template <int F>
-struct Fmt {
-    static constexpr int B =
-        (F == MX8_B16 || F == MX4_B16 || F == NV4_B16) ? 16 : (F == MX8_B32 || F == MX4_B32) ? 32 : 64;
-    static constexpr bool NV = F == NV4_B16;
-    static constexpr bool FP4 = F >= MX4_B16; // 4-bit codes
-    static constexpr int BL = B / 8;          // lanes (16-byte chunks) per block
-};
-
-// Chunks j*TL + l (j < cpl <= CPL) of `row` into v; zeros outside the tensor.
-template <int TL, int CPL>
-__device__ __forceinline__ void load_row(const Args &A, int64_t row, int l, int cpl,
-                                         uint4 (&v)[CPL])
-{
-    const bool row_ok = row < A.T;
-    const uint4 *xr = reinterpret_cast<const uint4 *>(A.x + (row_ok ? row : 0) * A.d);
-#pragma unroll
-    for (int j = 0; j < CPL; ++j) {
-        const int c = j * TL + l;
-        v[j] = (j < cpl && row_ok && c < A.nc) ? load_stream(xr + c) : make_uint4(0u, 0u, 0u, 0u);
-    }
-}
-
-// F: output format.  MXN: MXNorm (else RMSNorm).  GAM: apply gamma (RMSNorm
-// only).  Workgroup b handles rows b*TEAMS .. b*TEAMS+TEAMS-1, one per team.
-// (A persistent variant that prefetches each team's next row during the
-// current one needs about twice the registers; at the resulting occupancy it
-// was slower for five of the six MXFP8/NVFP4 kernels on MI355X.)
-template <int TL, int CPL, int F, bool MXN, bool GAM>
-__global__ void __launch_bounds__(Team<TL>::BLOCK)
-norm_cast_kernel(Args A)
-{
-    constexpr int BLOCK = Team<TL>::BLOCK;
-    constexpr int TEAMS = Team<TL>::TEAMS;
-    constexpr bool NV = Fmt<F>::NV;
-    constexpr bool FP4 = Fmt<F>::FP4;
-    constexpr int BL = Fmt<F>::BL; // lanes (chunks) per scale block
-    __shared__ double red[TL > 64 ? BLOCK / 64 : 1];
-    // the scale bytes of each row, gathered here and written with wide stores
-    constexpr int KMAX = TL * CPL / BL;
-    __shared__ __attribute__((aligned(16))) uint8_t sbuf[TEAMS * KMAX];
-    // NVFP4: for every finite E4M3 block scale S, den = RN(dec(S) s_g) and
-    // its correctly rounded reciprocal -- one IEEE division per entry per
-    // workgroup instead of one per block.  A zero reciprocal marks the scales
-    // whose blocks take the exact slow path (den = 0 or den < 2^-90).
-    __shared__ float2 den_tab[NV ? 128 : 1];
-    float six_sg = 0.0f, rcp_six_sg = 0.0f;
-    bool six_sg_ok = false;
-    if constexpr (NV) {
-        if (threadIdx.x < 127) {
-            const float den = e4m3_value(threadIdx.x) * A.s_g;
-            den_tab[threadIdx.x] = make_float2(den, den >= 0x1p-90f ? 1.0f / den : 0.0f);
-        }
-        six_sg = 6.0f * A.s_g;
-        rcp_six_sg = 1.0f / six_sg;
-        six_sg_ok = six_sg >= 0x1p-90f;
-        __syncthreads();
-    }
-
-    const int tid = threadIdx.x;
-    const int team = tid / TL;
-    const int l = tid - team * TL;
-    uint8_t *sb = sbuf + team * KMAX;
-
-    uint4 g[GAM ? CPL : 1]; // gamma chunks: the same columns for every row
-    if constexpr (GAM) {
-        const uint4 *gr = reinterpret_cast<const uint4 *>(A.gamma);
-#pragma unroll
-        for (int j = 0; j < CPL; ++j) {
-            const int c = j * TL + l;
-            g[j] = (c < A.nc) ? gr[c] : make_uint4(0u, 0u, 0u, 0u);
-        }
-    }
-
-    // chunks per lane this row actually has: the same for every lane, so the
-    // loops below skip the unused tail of the register array uniformly
-    const int cpl = (A.nc + TL - 1) / TL;
-    uint4 v[CPL];
-    {
-        const int64_t row = (int64_t)blockIdx.x * TEAMS + team;
-        load_row<TL, CPL>(A, row, l, cpl, v);
-        const bool row_ok = row < A.T;
-        const int64_t rr = row_ok ? row : 0;
-        bool ok[CPL];
-#pragma unroll
-        for (int j = 0; j < CPL; ++j)
-            ok[j] = row_ok && (j * TL + l) < A.nc;
-
-        // ---- pass 1: the row statistic ----
-        double s = 0.0;
-        uint32_t mb[MXN ? CPL : 1];
-        if constexpr (MXN) {
-#pragma unroll
-            for (int j = 0; j < CPL; ++j) {
-                if (j >= cpl)
-                    break;
-                const uint32_t m = block_max<BL>(chunk_absmax_bits(v[j]));
-                mb[j] = m;
-                // every lane of the block adds its term: the sum is BL times
-                // the block sum, removed exactly (BL is a power of two) below
-                const double md = (double)__uint_as_float(m << 16);
-                s += (A.p == 1) ? md : md * md;
-            }
-        } else {
-#pragma unroll
-            for (int j = 0; j < CPL; ++j) {
-                if (j >= cpl)
-                    break;
-                const uint32_t w[4] = {v[j].x, v[j].y, v[j].z, v[j].w};
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const double a = (double)bf16_lo(w[i]);
-                    const double b = (double)bf16_hi(w[i]);
-                    s = __builtin_fma(a, a, s);
-                    s = __builtin_fma(b, b, s);
-                }
-            }
-        }
-
-
-        // keep the row as raw bf16 between the passes rather than letting
-        // values converted in pass 1 stay live
-#pragma unroll
-        for (int j = 0; j < CPL; ++j)
-            asm volatile("" : "+v"(v[j].x), "+v"(v[j].y), "+v"(v[j].z), "+v"(v[j].w));
-        s = team_sum<TL>(s, red, tid);
-        if constexpr (MXN)
-            s *= 1.0 / BL;
-        const float rho =
-            MXN ? rho_estimate(s, A.K, A.p, A.coef, A.eps) : rho_rms(s, A.d, A.eps);
-        if (row_ok && l == 0 && A.rho)
-            A.rho[row] = rho;
-
-        // ---- pass 2: block scales and element codes ----
-#pragma unroll
-        for (int j = 0; j < CPL; ++j) {
-            if (j >= cpl)
-                break;
-            const int c = j * TL + l;
-            const uint32_t w[4] = {v[j].x, v[j].y, v[j].z, v[j].w};
-            float t[8];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                t[2 * i] = bf16_lo(w[i]) * rho;
-                t[2 * i + 1] = bf16_hi(w[i]) * rho;
-            }
-            if constexpr (GAM) {
-                const uint32_t gw[4] = {g[j].x, g[j].y, g[j].z, g[j].w};
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    t[2 * i] = t[2 * i] * bf16_lo(gw[i]);
-                    t[2 * i + 1] = t[2 * i + 1] * bf16_hi(gw[i]);
-                }
-            }
-            // block maximum of |t|
-            float a;
-            if constexpr (MXN) {
-                a = __uint_as_float(mb[j] << 16) * rho; // = max |t| (RN is monotone)
-            } else {
-                // integer max of the magnitude patterns: NaN propagates
-                uint32_t m = 0;
-#pragma unroll
-                for (int k = 0; k < 8; ++k)
-                    m = max(m, __float_as_uint(t[k]) & 0x7FFFFFFFu);
-                a = __uint_as_float(block_max<BL>(m));
-            }
-
-            if constexpr (!NV && !FP4) {
-                const uint32_t byte = e8m0_byte<false>(a, A.mode);
-                if (A.mode == MX_SCALE_FLOOR) {
-                    // |t| <= 448 * 2^e: saturate before the conversion
-                    const float lim = __uint_as_float(((byte + 8u) << 23) | 0x600000u);
-#pragma unroll
-                    for (int k = 0; k < 8; ++k)
-                        t[k] = __builtin_amdgcn_fmed3f(t[k], -lim, lim);
-                }
-                const float scale = __uint_as_float(byte << 23);
-                uint32_t lo = e4m3x4_hw(t[0], t[1], t[2], t[3], scale);
-                uint32_t hi = e4m3x4_hw(t[4], t[5], t[6], t[7], scale);
-                if (__builtin_amdgcn_ballot_w64(byte == 0xFFu)) { // rare: non-finite input
-                    if (byte == 0xFFu) {
-                        lo = nan_codes_e4m3(w[0], w[1]);
-                        hi = nan_codes_e4m3(w[2], w[3]);
-                    }
-                }
-                if (ok[j]) {
-                    *reinterpret_cast<uint2 *>(A.codes + rr * A.d + (int64_t)c * 8) =
-                        make_uint2(lo, hi);
-                    if ((l % BL) == 0)
-                        sb[c / BL] = (uint8_t)byte;
-                }
-            } else if constexpr (!NV) {
-                // MXFP4: E2M1 codes of t / 2^e.  The scaled fp4 conversion
-                // divides by the scale operand's power of two, rounds to
-                // nearest even and saturates at 6 (checked on the device on all
-                // fp32 inputs for scale exponents -127 .. 120), so FLOOR needs
-                // no clamp.
-                const uint32_t byte = e8m0_byte<true>(a, A.mode);
-                const float scale = __uint_as_float(byte << 23);
-                uint32_t packed = 0;
-                packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, t[0], t[1], scale, 0);
-                packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, t[2], t[3], scale, 1);
-                packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, t[4], t[5], scale, 2);
-                packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, t[6], t[7], scale, 3);
-                if (__builtin_amdgcn_ballot_w64(byte == 0xFFu)) { // rare: non-finite input
-                    if (byte == 0xFFu)
-                        packed = 0x77777777u | sign_nibbles(v[j]);
-                }
-                if (ok[j]) {
-                    *reinterpret_cast<uint32_t *>(A.codes + rr * (A.d / 2) + (int64_t)c * 4) =
-                        packed;
-                    if ((l % BL) == 0)
-                        sb[c / BL] = (uint8_t)byte;
-                }
-            } else {
-                uint32_t S, packed = 0;
-                if (!(a <= FLT_MAX)) { // NaN or Inf block maximum
-                    S = 0x7Fu;
-                    packed = 0x77777777u | sign_nibbles(v[j]);
-                } else {
-                    float q = six_sg_ok ? div_by_recip(a, six_sg, rcp_six_sg) : a / six_sg;
-                    if (q != q) // a is finite: a NaN here is an overflowed quotient
-                        q = __builtin_inff();
-                    // E4M3 code of q >= 0, nearest even, on the conversion
-                    // unit; the instruction gives NaN above 464 instead of
-                    // saturating, so clamp to 448 first
-                    S = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(__builtin_fminf(q, 448.0f),
-                                                                  0.0f, 0, false) & 0xFFu;
-                    const float2 dr = den_tab[S];
-                    const float den = dr.x, r = dr.y;
-                    if (r > 0.0f && a * r <= 0x1p100f) {
-                        // common case: every quotient is finite and the
-                        // Markstein correction is exact; the sign is taken
-                        // from t so zero and underflowing quotients keep it
-                        float vq[8];
-#pragma unroll
-                        for (int k = 0; k < 8; ++k)
-                            vq[k] = __builtin_copysignf(div_by_recip(t[k], den, r), t[k]);
-                        packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, vq[0], vq[1], 1.0f, 0);
-                        packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, vq[2], vq[3], 1.0f, 1);
-                        packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, vq[4], vq[5], 1.0f, 2);
-                        packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, vq[6], vq[7], 1.0f, 3);
-                    } else if (den == 0.0f) {
-#pragma unroll
-                        for (int k = 0; k < 8; ++k)
-                            packed |= ((__float_as_uint(t[k]) >> 31) << 3) << (4 * k);
-                    } else {
-#pragma unroll
-                        for (int k = 0; k < 8; ++k)
-                            packed |= e2m1_code(t[k] / den, t[k]) << (4 * k);
-                    }
-                }
-                if (ok[j]) {
-                    *reinterpret_cast<uint32_t *>(A.codes + rr * (A.d / 2) + (int64_t)c * 4) =
-                        packed;
-                    if ((l & 1) == 0)
-                        sb[c >> 1] = (uint8_t)S;
-                }
-            }
-        }
-
-        // ---- the row's K scale bytes: LDS -> one wide store per lane ----
-        if constexpr (TL > 64) {
-            __syncthreads();
-        } else {
-            // the team lives in one wave: order its LDS writes before the reads
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-            __builtin_amdgcn_wave_barrier();
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-        }
-        if (row_ok) {
-            uint8_t *dst = A.scales + rr * A.K;
-            if (A.sw == 16) {
-                if (l < A.K / 16)
-                    *reinterpret_cast<uint4 *>(dst + 16 * l) =
-                        *reinterpret_cast<const uint4 *>(sb + 16 * l);
-            } else if (A.sw == 4) {
-                for (int i = l; i < A.K / 4; i += TL)
-                    *reinterpret_cast<uint32_t *>(dst + 4 * i) =
-                        *reinterpret_cast<const uint32_t *>(sb + 4 * i);
-            } else {
-                for (int i = l; i < A.K; i += TL)
-                    dst[i] = sb[i];
-            }
-        }
-    }
-}
+using namespace mxk;
 
 // ------------------------------------------------------------ host side --
 
@@ -577,43 +88,6 @@ float table_coef(int block, int p)
     case 64: return p == 1 ? 0.3852f : 0.3803f;
     default: return NAN;
     }
-}
-
-template <int TL, int CPL, int F, bool MXN, bool GAM>
-hipError_t launch_one(const Args &A, hipStream_t stream)
-{
-    const int64_t blocks = (A.T + Team<TL>::TEAMS - 1) / Team<TL>::TEAMS;
-    hipLaunchKernelGGL((norm_cast_kernel<TL, CPL, F, MXN, GAM>), dim3((unsigned)blocks),
-                       dim3(Team<TL>::BLOCK), 0, stream, A);
-    return hipGetLastError();
-}
-
-template <int F, bool MXN, bool GAM>
-hipError_t launch_kind(const Args &A, int TL, int CPL, hipStream_t stream)
-{
-#define MXN_CASE(tl)                                                                     \
-    case tl:                                                                             \
-        return CPL == 4 ? launch_one<tl, 4, F, MXN, GAM>(A, stream)                      \
-                        : launch_one<tl, 8, F, MXN, GAM>(A, stream);
-    switch (TL) {
-        MXN_CASE(16)
-        MXN_CASE(32)
-        MXN_CASE(64)
-        MXN_CASE(128)
-        MXN_CASE(256)
-        MXN_CASE(512)
-    }
-#undef MXN_CASE
-    return hipErrorInvalidValue;
-}
-
-template <int F>
-hipError_t launch_fmt(const Args &A, bool mxn, int TL, int CPL, hipStream_t stream)
-{
-    if (mxn)
-        return launch_kind<F, true, false>(A, TL, CPL, stream);
-    return A.gamma ? launch_kind<F, false, true>(A, TL, CPL, stream)
-                   : launch_kind<F, false, false>(A, TL, CPL, stream);
 }
 
 // Team size (lanes per row, 16 .. 512) and register chunks per lane (4 or 8).
@@ -673,7 +147,7 @@ mx_status check_global_scale(float s_g)
     return MX_OK;
 }
 
-mx_status run(Args A, int fmt, bool mxn, void *stream)
+mx_status run(Args A, int fmt, int kind, void *stream)
 {
     int TL, CPL;
     pick_team(A.T, A.nc, TL, CPL);
@@ -687,16 +161,9 @@ mx_status run(Args A, int fmt, bool mxn, void *stream)
     A.sw = (A.K % 16 == 0 && sa % 16 == 0) ? 16 : (A.K % 4 == 0 && sa % 4 == 0) ? 4 : 1;
     hipStream_t st = (hipStream_t)stream;
     hipError_t e;
-    switch (fmt) {
-    case MX8_B16: e = launch_fmt<MX8_B16>(A, mxn, TL, CPL, st); break;
-    case MX8_B32: e = launch_fmt<MX8_B32>(A, mxn, TL, CPL, st); break;
-    case MX8_B64: e = launch_fmt<MX8_B64>(A, mxn, TL, CPL, st); break;
-    case MX4_B16: e = launch_fmt<MX4_B16>(A, mxn, TL, CPL, st); break;
-    case MX4_B32: e = launch_fmt<MX4_B32>(A, mxn, TL, CPL, st); break;
-    case MX4_B64: e = launch_fmt<MX4_B64>(A, mxn, TL, CPL, st); break;
-    case NV4_B16: e = launch_fmt<NV4_B16>(A, mxn, TL, CPL, st); break;
-    default: return fail(MX_EINVAL, "unknown output format");
-    }
+    if (fmt < MX8_B16 || fmt > NV4_B16)
+        return fail(MX_EINVAL, "unknown output format");
+    e = launch_norm_cast(fmt, A, kind, TL, CPL, st);
     if (e != hipSuccess)
         return fail(MX_EHIP, "kernel launch failed: %s", hipGetErrorString(e));
     return MX_OK;
@@ -767,7 +234,7 @@ mx_status mxnorm_mxfp8_fwd(const void *x, int64_t T, int64_t d, int p, float coe
         return fail(MX_EINVAL, "unknown scale_mode %d", scale_mode);
     return run(make_args(x, nullptr, T, d, 32, p, coef, eps, scale_mode, 1.0f, codes, scales,
                          rho),
-               MX8_B32, true, stream);
+               MX8_B32, K_MXN, stream);
 }
 
 mx_status rmsnorm_mxfp8_fwd(const void *x, const void *gamma, int64_t T, int64_t d, float eps,
@@ -782,7 +249,7 @@ mx_status rmsnorm_mxfp8_fwd(const void *x, const void *gamma, int64_t T, int64_t
         return fail(MX_EINVAL, "unknown scale_mode %d", scale_mode);
     return run(make_args(x, gamma, T, d, 32, 2, 1.0f, eps, scale_mode, 1.0f, codes, scales,
                          rho),
-               MX8_B32, false, stream);
+               MX8_B32, K_RMS, stream);
 }
 
 mx_status mxnorm_nvfp4_fwd(const void *x, int64_t T, int64_t d, int p, float coef, float eps,
@@ -799,7 +266,7 @@ mx_status mxnorm_nvfp4_fwd(const void *x, int64_t T, int64_t d, int p, float coe
         return st;
     return run(make_args(x, nullptr, T, d, 16, p, coef, eps, MX_SCALE_RCEIL, global_scale,
                          codes, scales, rho),
-               NV4_B16, true, stream);
+               NV4_B16, K_MXN, stream);
 }
 
 mx_status rmsnorm_nvfp4_fwd(const void *x, const void *gamma, int64_t T, int64_t d, float eps,
@@ -814,7 +281,7 @@ mx_status rmsnorm_nvfp4_fwd(const void *x, const void *gamma, int64_t T, int64_t
         return st;
     return run(make_args(x, gamma, T, d, 16, 2, 1.0f, eps, MX_SCALE_RCEIL, global_scale, codes,
                          scales, rho),
-               NV4_B16, false, stream);
+               NV4_B16, K_RMS, stream);
 }
 
 mx_status mxnorm_mx_fwd(const void *x, int64_t T, int64_t d, int block, int elem, int p,
@@ -834,7 +301,7 @@ mx_status mxnorm_mx_fwd(const void *x, int64_t T, int64_t d, int block, int elem
         return fail(MX_EINVAL, "unknown scale_mode %d", scale_mode);
     return run(make_args(x, nullptr, T, d, block, p, coef, eps, scale_mode, 1.0f, codes, scales,
                          rho),
-               fmt, true, stream);
+               fmt, K_MXN, stream);
 }
 
 mx_status rmsnorm_mx_fwd(const void *x, const void *gamma, int64_t T, int64_t d, int block,
@@ -852,7 +319,24 @@ mx_status rmsnorm_mx_fwd(const void *x, const void *gamma, int64_t T, int64_t d,
         return fail(MX_EINVAL, "unknown scale_mode %d", scale_mode);
     return run(make_args(x, gamma, T, d, block, 2, 1.0f, eps, scale_mode, 1.0f, codes, scales,
                          rho),
-               fmt, false, stream);
+               fmt, K_RMS, stream);
+}
+
+mx_status mx_cast_fwd(const void *x, const void *gamma, int64_t T, int64_t d, int block,
+                      int elem, int scale_mode, uint8_t *codes, uint8_t *scales, void *stream)
+{
+    g_err[0] = '\0';
+    const int fmt = mx_format(block, elem);
+    if (fmt < 0)
+        return fail(MX_EINVAL, "block must be 16, 32 or 64 and elem E4M3 or E2M1");
+    mx_status st = check_common(x, gamma, T, d, block, 0.0f, codes, scales, nullptr);
+    if (st != MX_OK)
+        return st;
+    if (scale_mode != MX_SCALE_RCEIL && scale_mode != MX_SCALE_FLOOR)
+        return fail(MX_EINVAL, "unknown scale_mode %d", scale_mode);
+    return run(make_args(x, gamma, T, d, block, 2, 1.0f, 0.0f, scale_mode, 1.0f, codes, scales,
+                         nullptr),
+               fmt, K_CAST, stream);
 }
 
 float mxnorm_default_global_scale(int64_t d, int block, int p, float coef)

@@ -1,0 +1,12 @@
+// norm_cast_f3.hip -- instantiates the norm + cast kernels for output format
+// MX4_B16 (one translation unit per format keeps the build parallel).
+#include "norm_cast.h"
+
+namespace mxk {
+
+hipError_t launch_norm_cast_MX4_B16(const Args &A, int kind, int TL, int CPL, hipStream_t stream)
+{
+    return launch_fmt<MX4_B16>(A, kind, TL, CPL, stream);
+}
+
+} // namespace mxk

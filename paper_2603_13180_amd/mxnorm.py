@@ -50,6 +50,7 @@ def load():
         "rmsnorm_nvfp4_fwd": (I, [P, P, I64, I64, F, F, P, P, P, P]),
         "mxnorm_mx_fwd": (I, [P, I64, I64, I, I, I, F, F, I, P, P, P, P]),
         "rmsnorm_mx_fwd": (I, [P, P, I64, I64, I, I, F, I, P, P, P, P]),
+        "mx_cast_fwd": (I, [P, P, I64, I64, I, I, I, P, P, P]),
         "mxnorm_default_global_scale": (F, [I64, I, I, F]),
         "rmsnorm_default_global_scale": (F, [I64, F]),
         "mxnorm_coef": (F, [I, I]),
@@ -212,6 +213,22 @@ def rmsnorm_mx_fwd(x, gamma=None, block=32, elem="e4m3", eps=1e-6, scale_mode="r
                                  SCALE_MODES[scale_mode], _ptr(codes), _ptr(scales),
                                  _ptr(rho) if want_rho else None, _stream(x.device)))
     return codes, scales, (rho if want_rho else None)
+
+
+def mx_cast_fwd(x, gamma=None, block=32, elem="e4m3", scale_mode="rceil",
+                codes=None, scales=None):
+    """Plain MX cast of x (or RN(x * gamma)), no normalisation.  With x a
+    weight [N, d] and gamma the norm gain this is the gain-folded weight cast
+    of the MXNormLinear forward (Sec. 3.7)."""
+    T, d = _input(x)
+    g = _gamma(gamma, x)
+    cs, ss = _mx_out_shapes(T, d, block, elem)
+    codes = _out(codes, cs, torch.uint8, x.device)
+    scales = _out(scales, ss, torch.uint8, x.device)
+    _check(load().mx_cast_fwd(_ptr(x), _ptr(g), T, d, block, ELEMS[elem],
+                              SCALE_MODES[scale_mode], _ptr(codes), _ptr(scales),
+                              _stream(x.device)))
+    return codes, scales
 
 
 def mxnorm_default_global_scale(d, block=16, p=2, coef=0.0):

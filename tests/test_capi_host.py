@@ -168,3 +168,15 @@ def test_generic_mx_entry_points_validate(args, status):
                              OUT if T else None, None, None) == status
     assert lib.rmsnorm_mx_fwd(x, None, T, d, block, elem, 1e-6, 0, OUT if T else None,
                               OUT if T else None, None, None) == status
+    assert lib.mx_cast_fwd(x, None, T, d, block, elem, 0, OUT if T else None,
+                           OUT if T else None, None) == status
+
+
+def test_mx_cast_rejects_bad_arguments():
+    lib = mxnorm.load()
+    ok = (A16, None, 4, 64, 32, 0, 0, OUT, OUT, None)
+    assert lib.mx_cast_fwd(*ok[:1], A8, *ok[2:]) == 1              # gamma alignment
+    assert lib.mx_cast_fwd(*ok[:6], 2, *ok[7:]) == 1               # scale mode
+    assert lib.mx_cast_fwd(None, *ok[1:]) == 1                     # x NULL with T > 0
+    assert lib.mx_cast_fwd(*ok[:7], None, *ok[8:]) == 1            # codes NULL
+    assert lib.mx_cast_fwd(*ok[:2], -1, *ok[3:]) == 1              # T < 0

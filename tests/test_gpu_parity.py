@@ -468,3 +468,39 @@ def test_mx_b32_e4m3_equals_mxfp8_entry_point():
     torch.cuda.synchronize()
     for u, v in zip(a, b):
         assert torch.equal(u, v)
+
+
+# ------------------------------------------- gain-folded weight cast --
+
+def check_cast(wb, gb, block, elem, mode="rceil"):
+    w = dev_bf16(wb)
+    g = None if gb is None else dev_bf16(gb)
+    codes, scales = mxnorm.mx_cast_fwd(w, g, block=block, elem=elem, scale_mode=mode)
+    torch.cuda.synchronize()
+    wc, ws = oracle.mxcast_gain(wb, gb, B=block, elem=elem, mode=mode)
+    ctx = "cast B=%d %s %s shape=%s gamma=%s" % (block, elem, mode, wb.shape, gb is not None)
+    s, c = scales.cpu().numpy(), codes.cpu().numpy()
+    bad = np.argwhere(s != ws)
+    assert bad.size == 0, "%s: %d scale bytes differ, first %s" % (ctx, len(bad), bad[0])
+    bad = np.argwhere(c != wc)
+    assert bad.size == 0, "%s: %d codes differ, first %s" % (ctx, len(bad), bad[0])
+
+
+@pytest.mark.parametrize("block,elem", MX_FORMATS)
+@pytest.mark.parametrize("N,d", [(1, 64), (67, 192), (130, 1024), (257, 4096), (5, 14336)])
+def test_weight_cast_with_folded_gain(block, elem, N, d):
+    # weights of a linear layer: small Gaussian entries; gain around 1
+    wb = synth.gaussian(N, d, seed=N * d + block, scale=0.02)
+    gb = synth.f32_to_bf16_bits(np.random.default_rng(d).uniform(0.2, 3.0, d).astype(np.float32))
+    for mode in ("rceil", "floor"):
+        check_cast(wb, gb, block, elem, mode)
+        check_cast(wb, None, block, elem, mode)
+
+
+@pytest.mark.parametrize("block,elem", MX_FORMATS)
+def test_weight_cast_edge_rows(block, elem):
+    for d in (64, 1024):
+        ab = adversarial_rows(d, seed=d + block)
+        gb = synth.f32_to_bf16_bits(np.linspace(-3, 3, d).astype(np.float32))
+        check_cast(ab, gb, block, elem)
+        check_cast(ab, None, block, elem, "floor")
