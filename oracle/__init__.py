@@ -77,7 +77,7 @@ def _load():
         "mxo_mxnorm_mx": (None, [P, I64, I64, I, I, I, F, F, I, P, P, P, P]),
         "mxo_rmsnorm_mx": (None, [P, P, I64, I64, I, I, F, I, P, P, P, P]),
         "mxo_mxcast_gain": (None, [P, P, I64, I64, I, I, I, P, P]),
-        "mxo_mx_matmul": (None, [P, P, P, P, I64, I64, I64, I, I, P]),
+        "mxo_mx_matmul": (ctypes.c_int, [P, P, P, P, I64, I64, I64, I, I, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -326,8 +326,9 @@ def mx_matmul(a_codes, a_scales, b_codes, b_scales, K, B=32, elem="e4m3"):
     b_scales = np.ascontiguousarray(b_scales, np.uint8)
     M, N = a_codes.shape[0], b_codes.shape[0]
     h = np.empty((M, N), np.float64)
-    _load().mxo_mx_matmul(_ptr(a_codes), _ptr(a_scales), _ptr(b_codes), _ptr(b_scales), M, N, K,
-                          B, ELEMS[elem], _ptr(h))
+    if _load().mxo_mx_matmul(_ptr(a_codes), _ptr(a_scales), _ptr(b_codes), _ptr(b_scales), M, N,
+                             K, B, ELEMS[elem], _ptr(h)) != 0:
+        raise MemoryError("mx_matmul: cannot allocate the decoded operand")
     return h
 
 

@@ -62,6 +62,7 @@
  */
 #include <math.h>
 #include <stdint.h>
+#include <stdlib.h>
 #include <string.h>
 
 #define MXO_SCALE_RCEIL 0
@@ -667,20 +668,33 @@ static double mx_element(const uint8_t *codes_row, const uint8_t *scales_row, in
 
 /* H = A B^T for MX matrices A [M, K] and B [N, K] (both blocked along K):
  * H[m][n] = sum_k dec(A)[m][k] dec(B)[n][k], the matmul of eq. (mx-matmul)
- * "accumulated in higher precision" -- here in double, in index order. */
-void mxo_mx_matmul(const uint8_t *a_codes, const uint8_t *a_scales, const uint8_t *b_codes,
-                   const uint8_t *b_scales, int64_t M, int64_t N, int64_t K, int B, int elem,
-                   double *h)
+ * "accumulated in higher precision" -- here in double, in index order.  Rows
+ * are decoded to double once (dec(B) whole, dec(A) a row at a time); returns
+ * 0, or -1 if that buffer cannot be allocated. */
+int mxo_mx_matmul(const uint8_t *a_codes, const uint8_t *a_scales, const uint8_t *b_codes,
+                  const uint8_t *b_scales, int64_t M, int64_t N, int64_t K, int B, int elem,
+                  double *h)
 {
     const int64_t cw = elem == MXO_ELEM_E2M1 ? K / 2 : K, sw = K / B;
     int64_t m, n, k;
+    double *db = malloc(sizeof(double) * (size_t)(N * K + K));
+    double *da;
+    if (!db)
+        return -1;
+    da = db + N * K;
+    for (n = 0; n < N; n++)
+        for (k = 0; k < K; k++)
+            db[n * K + k] = mx_element(b_codes + n * cw, b_scales + n * sw, k, B, elem);
     for (m = 0; m < M; m++) {
+        for (k = 0; k < K; k++)
+            da[k] = mx_element(a_codes + m * cw, a_scales + m * sw, k, B, elem);
         for (n = 0; n < N; n++) {
             double s = 0.0;
             for (k = 0; k < K; k++)
-                s += mx_element(a_codes + m * cw, a_scales + m * sw, k, B, elem) *
-                     mx_element(b_codes + n * cw, b_scales + n * sw, k, B, elem);
+                s += da[k] * db[n * K + k];
             h[m * N + n] = s;
         }
     }
+    free(db);
+    return 0;
 }
