@@ -40,6 +40,9 @@ def parse():
     ap.add_argument("--sweep", metavar="OUT_JSON",
                     help="instead of the headline line, run the paper's kernel sweep "
                          "(17 hidden sizes x 5 token counts) and write per-shape results")
+    ap.add_argument("--layer", metavar="OUT_JSON",
+                    help="instead of the headline line, run the MXNormLinear layer benchmark "
+                         "(norm + MX matmul at Llama-3-8B projection shapes) and write results")
     ap.add_argument("--sweep-formats",
                     default="e4m3-b32,nvfp4,e4m3-b16,e4m3-b64,e2m1-b16,e2m1-b32,e2m1-b64",
                     help="comma list of e4m3-b{16,32,64}, e2m1-b{16,32,64}, nvfp4")
@@ -155,6 +158,119 @@ def run_sweep(path, formats):
     print(json.dumps({"sweep": path, "summary": summary}))
 
 
+# MI355X dense matrix-core peaks (TFLOP/s) for the MX matmul's element types
+PEAK_MFMA_TFLOPS = {"e4m3": 5000.0, "e2m1": 10100.0}
+LAYER_D = 4096                       # Llama-3-8B hidden size
+LAYER_N = {"qkv": 6144, "gate_up": 28672}   # projections that follow a norm
+LAYER_T = [4096, 8192, 16384, 32768, 65536]
+
+
+def layer_case(fmt, T, N, stream, gen, rounds=3, budget_ms=40.0):
+    """One MXNormLinear shape: MXNorm -> MX matmul against RMSNorm (gain) +
+    MX cast -> the same matmul, each pair captured as one graph and timed in
+    interleaved rounds.  Returns a result dict."""
+    import numpy as np
+    import torch
+    from paper_2603_13180_amd import mxnorm
+
+    dev = torch.device("cuda:0")
+    d = LAYER_D
+    x = torch.randn(T, d, generator=gen, device=dev).to(torch.bfloat16)
+    w = (0.02 * torch.randn(N, d, generator=gen, device=dev)).to(torch.bfloat16)
+    gam = (1.0 + 0.1 * torch.randn(d, generator=gen, device=dev)).to(torch.bfloat16)
+    wc_g, ws_g = mxnorm.mx_cast_fwd(w, gam, block=32, elem=fmt)   # MXCast(W gamma)
+    wc, ws = mxnorm.mx_cast_fwd(w, None, block=32, elem=fmt)      # MXCast(W)
+    cw = d if fmt == "e4m3" else d // 2
+    codes = torch.empty(T, cw, dtype=torch.uint8, device=dev)
+    scales = torch.empty(T, d // 32, dtype=torch.uint8, device=dev)
+    out = torch.empty(T, N, dtype=torch.bfloat16, device=dev)
+
+    def mx_layer(_):
+        mxnorm.mxnorm_mx_fwd(x, 32, fmt, codes=codes, scales=scales, want_rho=False)
+        mxnorm.mx_matmul_fwd(codes, scales, wc_g, ws_g, d, elem=fmt, out_dtype=torch.bfloat16,
+                             out=out)
+
+    def rms_layer(_):
+        mxnorm.rmsnorm_mx_fwd(x, gam, 32, fmt, codes=codes, scales=scales, want_rho=False)
+        mxnorm.mx_matmul_fwd(codes, scales, wc, ws, d, elem=fmt, out_dtype=torch.bfloat16,
+                             out=out)
+
+    def gemm(_):
+        mxnorm.mx_matmul_fwd(codes, scales, wc, ws, d, elem=fmt, out_dtype=torch.bfloat16,
+                             out=out)
+
+    def mx_norm(_):
+        mxnorm.mxnorm_mx_fwd(x, 32, fmt, codes=codes, scales=scales, want_rho=False)
+
+    def rms_norm(_):
+        mxnorm.rmsnorm_mx_fwd(x, gam, 32, fmt, codes=codes, scales=scales, want_rho=False)
+
+    flops = 2.0 * T * N * d
+    est_ms = flops / 1.5e15 * 1e3
+    reps = max(2, int(budget_ms / est_ms))
+    t = {k: [] for k in ("mx", "rms", "gemm", "mx_norm", "rms_norm")}
+    for _ in range(rounds):
+        t["mx"].append(graph_time(mx_layer, 1, reps, 1, stream))
+        t["rms"].append(graph_time(rms_layer, 1, reps, 1, stream))
+        t["gemm"].append(graph_time(gemm, 1, reps, 1, stream))
+        t["mx_norm"].append(graph_time(mx_norm, 1, 4 * reps, 1, stream))
+        t["rms_norm"].append(graph_time(rms_norm, 1, 4 * reps, 1, stream))
+    m = {k: float(np.median(v)) for k, v in t.items()}
+    tf = flops / (m["gemm"] * 1e-3) / 1e12
+    del x, w, codes, scales, out, wc, ws, wc_g, ws_g
+    torch.cuda.empty_cache()
+    return {"format": fmt, "tokens": T, "N": N, "d": d,
+            "mxnorm_linear_us": round(m["mx"] * 1e3, 2),
+            "rmsnorm_cast_linear_us": round(m["rms"] * 1e3, 2),
+            "layer_speedup": round(m["rms"] / m["mx"], 4),
+            # the matmul is common to both layers: the same ratio from the
+            # separately timed parts, free of the matmul's run-to-run noise
+            "layer_speedup_from_parts":
+                round((m["rms_norm"] + m["gemm"]) / (m["mx_norm"] + m["gemm"]), 4),
+            "matmul_us": round(m["gemm"] * 1e3, 2),
+            "matmul_TFLOPs": round(tf, 1),
+            "matmul_frac_of_peak": round(tf / PEAK_MFMA_TFLOPS[fmt], 4),
+            "mxnorm_us": round(m["mx_norm"] * 1e3, 2),
+            "rmsnorm_gamma_cast_us": round(m["rms_norm"] * 1e3, 2)}
+
+
+def run_layer(path):
+    """The MXNormLinear forward at the Llama-3-8B projections that consume a
+    norm (QKV and gate+up, d = 4096) over the paper's token counts, MXFP8 and
+    MXFP4 (E8M0 scales, 32-element blocks)."""
+    import math
+    import torch
+    from paper_2603_13180_amd import mxnorm
+
+    mxnorm.load()
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.Stream(dev)
+    gen = torch.Generator(device=dev)
+    results, summary = [], {}
+    for fmt in ("e4m3", "e2m1"):
+        sp, spp = [], []
+        for name, N in LAYER_N.items():
+            for T in LAYER_T:
+                gen.manual_seed(T * 31 + N)
+                r = layer_case(fmt, T, N, stream, gen)
+                r["projection"] = name
+                results.append(r)
+                sp.append(r["layer_speedup"])
+                spp.append(r["layer_speedup_from_parts"])
+                print(json.dumps(r), file=sys.stderr, flush=True)
+        gm = lambda v: round(math.exp(sum(math.log(u) for u in v) / len(v)), 4)
+        summary[fmt] = {"geomean_layer_speedup": gm(sp), "min": min(sp), "max": max(sp),
+                        "geomean_layer_speedup_from_parts": gm(spp), "shapes": len(sp)}
+    doc = {"method": "each layer variant (norm kernel + MX matmul, bf16 output) captured as a "
+                     "HIP graph, replayed ~40 ms per round, median of 3 interleaved rounds; "
+                     "RMSNorm path applies the gain and multiplies MXCast(W), the MXNorm path "
+                     "multiplies MXCast(W gamma); N(0,1) activations, 0.02 N(0,1) weights",
+           "summary": summary, "results": results}
+    with open(path, "w") as f:
+        json.dump(doc, f, indent=1)
+    print(json.dumps({"layer": path, "summary": summary}))
+
+
 def mxfp8_bytes(T, d):
     return T * d * 2 + T * d + T * (d // 32) + 4 * T
 
@@ -227,6 +343,9 @@ def main():
     args = parse()
     if args.sweep:
         run_sweep(args.sweep, args.sweep_formats.split(","))
+        return
+    if args.layer:
+        run_layer(args.layer)
         return
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
@@ -319,6 +438,13 @@ def main():
     m = time_launches(lambda i: dst.copy_(xs[i]), n_sets, 50, 5, stream)
     copy_gbps = 2 * x0.numel() * 2 / (m * 1e-3) / 1e9
 
+    # the MX matmul the MXNorm output feeds (Llama-3-8B QKV projection)
+    del ncodes, nscales, small
+    torch.cuda.empty_cache()
+    lgen = torch.Generator(device=dev)
+    lgen.manual_seed(7)
+    lay = layer_case("e4m3", T, LAYER_N["qkv"], torch.cuda.Stream(dev), lgen)
+
     traffic = measured_traffic()
     line = {
         "metric": "MXNorm+MXFP8 cast HBM GB/s (% of peak); speedup vs RMSNorm+cast",
@@ -356,6 +482,11 @@ def main():
                 round(side["rmsnorm_nvfp4_gamma"]["ms"] / side["mxnorm_nvfp4"]["ms"], 4),
         },
         "kernels": side,
+        "mx_matmul": {
+            "shape": "MXNormLinear QKV: [%d, %d] x [%d, %d]^T MXFP8 -> bf16" % (T, d, lay["N"], d),
+            "TFLOP/s": lay["matmul_TFLOPs"], "frac_of_fp8_peak": lay["matmul_frac_of_peak"],
+            "layer_speedup_vs_rmsnorm_gamma_cast": lay["layer_speedup"],
+            "layer_speedup_from_parts": lay["layer_speedup_from_parts"]},
         "copy_d2d_GBps": round(copy_gbps, 1),
         "stream_reference_GBps": ref,
         "frac_of_stream_reference": round(gbps / ref["mixed"], 4),

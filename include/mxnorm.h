@@ -54,6 +54,7 @@ extern "C" {
 
 #define MXNORM_ABI_VERSION 1
 #define MXNORM_MAX_D 32768
+#define MX_MATMUL_MAX_K (1 << 22)
 
 typedef enum {
     MX_OK = 0,
@@ -151,6 +152,36 @@ mx_status rmsnorm_mx_fwd(const void *x, const void *gamma, int64_t T, int64_t d,
  */
 mx_status mx_cast_fwd(const void *x, const void *gamma, int64_t T, int64_t d, int block,
                       int elem, int scale_mode, uint8_t *codes, uint8_t *scales, void *stream);
+
+typedef enum {
+    MX_OUT_F32 = 0,       /* float32 output */
+    MX_OUT_BF16 = 1       /* bfloat16 output, rounded to nearest even */
+} mx_out_dtype;
+
+/*
+ * The MX matrix product of the MXNormLinear forward (Sec. 3.7 eq.
+ * (mx-matmul)):  H = dec(A) dec(B)^T,  H[m][n] = sum_k A[m][k] B[n][k],
+ * where A is an activation [M, K] (e.g. the output of mxnorm_mx_fwd) and B a
+ * weight [N, K] (e.g. the output of mx_cast_fwd), both MX-encoded along K:
+ * codes uint8 [rows, K] (E4M3) or [rows, K/2] (E2M1, two per byte, element
+ * 2j in the low nibble) and E8M0 scales uint8 [rows, K/block], row-major,
+ * device pointers.  out: device [M, N] row-major, float32 or bf16
+ * (mx_out_dtype), written entirely; owned by the caller.
+ * The product runs on the block-scaled matrix cores: each 32-element block's
+ * scales are applied exactly, products of the elements are exact, and the
+ * sum is accumulated in float32 with the matrix core's own rounding (within
+ * one instruction, products far below the largest one can be dropped; the
+ * total error stays within 2^-9 of sum_k |A[m][k] B[n][k]|).  A NaN scale or
+ * code gives NaN; results beyond the float range are infinite.
+ * block: 32 (other sizes: MX_EUNSUPPORTED).  elem: mx_elem.  Requirements:
+ * K a multiple of 128 (E4M3) or 256 (E2M1) and at most MX_MATMUL_MAX_K, N a
+ * multiple of 16 (else MX_EUNSUPPORTED); codes 16-byte, scales 4-byte, out 16-byte (f32) or
+ * 8-byte (bf16) aligned.  M == 0 or N == 0 is a no-op.  Asynchronous on
+ * `stream`; nothing is allocated.
+ */
+mx_status mx_matmul_fwd(const uint8_t *a_codes, const uint8_t *a_scales, const uint8_t *b_codes,
+                        const uint8_t *b_scales, int64_t M, int64_t N, int64_t K, int block,
+                        int elem, int out_dtype, void *out, void *stream);
 
 /*
  * Default NVFP4 tensor decode scales: an output bound divided by 6 * 448, so

@@ -32,6 +32,7 @@
 
 #include "mxnorm.h"
 #include "norm_cast.h"
+#include "status.h"
 
 namespace mxk {
 
@@ -57,14 +58,6 @@ hipError_t launch_norm_cast(int fmt, const Args &A, int kind, int TL, int CPL, h
     }
 }
 
-} // namespace mxk
-
-namespace {
-
-using namespace mxk;
-
-// ------------------------------------------------------------ host side --
-
 thread_local char g_err[256] = "";
 
 mx_status fail(mx_status st, const char *fmt, ...)
@@ -75,6 +68,18 @@ mx_status fail(mx_status st, const char *fmt, ...)
     va_end(ap);
     return st;
 }
+
+void clear_error() { g_err[0] = '\0'; }
+
+const char *last_error() { return g_err; }
+
+} // namespace mxk
+
+namespace {
+
+using namespace mxk;
+
+// ------------------------------------------------------------ host side --
 
 bool aligned(const void *p, uintptr_t n) { return ((uintptr_t)p % n) == 0; }
 
@@ -224,7 +229,7 @@ mx_status mxnorm_mxfp8_fwd(const void *x, int64_t T, int64_t d, int p, float coe
                            int scale_mode, uint8_t *codes, uint8_t *scales, float *rho,
                            void *stream)
 {
-    g_err[0] = '\0';
+    clear_error();
     mx_status st = check_common(x, nullptr, T, d, 32, eps, codes, scales, rho);
     if (st != MX_OK)
         return st;
@@ -241,7 +246,7 @@ mx_status rmsnorm_mxfp8_fwd(const void *x, const void *gamma, int64_t T, int64_t
                             int scale_mode, uint8_t *codes, uint8_t *scales, float *rho,
                             void *stream)
 {
-    g_err[0] = '\0';
+    clear_error();
     mx_status st = check_common(x, gamma, T, d, 32, eps, codes, scales, rho);
     if (st != MX_OK)
         return st;
@@ -256,7 +261,7 @@ mx_status mxnorm_nvfp4_fwd(const void *x, int64_t T, int64_t d, int p, float coe
                            float global_scale, uint8_t *codes, uint8_t *scales, float *rho,
                            void *stream)
 {
-    g_err[0] = '\0';
+    clear_error();
     mx_status st = check_common(x, nullptr, T, d, 16, eps, codes, scales, rho);
     if (st != MX_OK)
         return st;
@@ -273,7 +278,7 @@ mx_status rmsnorm_nvfp4_fwd(const void *x, const void *gamma, int64_t T, int64_t
                             float global_scale, uint8_t *codes, uint8_t *scales, float *rho,
                             void *stream)
 {
-    g_err[0] = '\0';
+    clear_error();
     mx_status st = check_common(x, gamma, T, d, 16, eps, codes, scales, rho);
     if (st != MX_OK)
         return st;
@@ -288,7 +293,7 @@ mx_status mxnorm_mx_fwd(const void *x, int64_t T, int64_t d, int block, int elem
                         float coef, float eps, int scale_mode, uint8_t *codes, uint8_t *scales,
                         float *rho, void *stream)
 {
-    g_err[0] = '\0';
+    clear_error();
     const int fmt = mx_format(block, elem);
     if (fmt < 0)
         return fail(MX_EINVAL, "block must be 16, 32 or 64 and elem E4M3 or E2M1");
@@ -308,7 +313,7 @@ mx_status rmsnorm_mx_fwd(const void *x, const void *gamma, int64_t T, int64_t d,
                          int elem, float eps, int scale_mode, uint8_t *codes, uint8_t *scales,
                          float *rho, void *stream)
 {
-    g_err[0] = '\0';
+    clear_error();
     const int fmt = mx_format(block, elem);
     if (fmt < 0)
         return fail(MX_EINVAL, "block must be 16, 32 or 64 and elem E4M3 or E2M1");
@@ -325,7 +330,7 @@ mx_status rmsnorm_mx_fwd(const void *x, const void *gamma, int64_t T, int64_t d,
 mx_status mx_cast_fwd(const void *x, const void *gamma, int64_t T, int64_t d, int block,
                       int elem, int scale_mode, uint8_t *codes, uint8_t *scales, void *stream)
 {
-    g_err[0] = '\0';
+    clear_error();
     const int fmt = mx_format(block, elem);
     if (fmt < 0)
         return fail(MX_EINVAL, "block must be 16, 32 or 64 and elem E4M3 or E2M1");
@@ -370,7 +375,7 @@ const char *mx_status_str(mx_status s)
     return "unknown mx_status";
 }
 
-const char *mx_last_error(void) { return g_err; }
+const char *mx_last_error(void) { return mxk::last_error(); }
 
 int mxnorm_abi_version(void) { return MXNORM_ABI_VERSION; }
 

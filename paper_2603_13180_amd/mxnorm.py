@@ -16,6 +16,7 @@ LIB_PATH = os.path.join(_HERE, "libmxnorm.so")
 
 MX_OK, MX_EINVAL, MX_EUNSUPPORTED, MX_EHIP = 0, 1, 2, 3
 SCALE_MODES = {"rceil": 0, "floor": 1}
+OUT_DTYPES = {torch.float32: 0, torch.bfloat16: 1}
 ELEMS = {"e4m3": 0, "e2m1": 1}
 ABI_VERSION = 1
 MAX_D = 32768
@@ -51,6 +52,7 @@ def load():
         "mxnorm_mx_fwd": (I, [P, I64, I64, I, I, I, F, F, I, P, P, P, P]),
         "rmsnorm_mx_fwd": (I, [P, P, I64, I64, I, I, F, I, P, P, P, P]),
         "mx_cast_fwd": (I, [P, P, I64, I64, I, I, I, P, P, P]),
+        "mx_matmul_fwd": (I, [P, P, P, P, I64, I64, I64, I, I, I, P, P]),
         "mxnorm_default_global_scale": (F, [I64, I, I, F]),
         "rmsnorm_default_global_scale": (F, [I64, F]),
         "mxnorm_coef": (F, [I, I]),
@@ -229,6 +231,46 @@ def mx_cast_fwd(x, gamma=None, block=32, elem="e4m3", scale_mode="rceil",
                               SCALE_MODES[scale_mode], _ptr(codes), _ptr(scales),
                               _stream(x.device)))
     return codes, scales
+
+
+def _mx_operand(codes, scales, K, block, elem, name):
+    cw = K if elem == "e4m3" else K // 2
+    for t, shape_ok in ((codes, codes.dim() == 2 and codes.shape[1] == cw),
+                        (scales, scales.dim() == 2 and scales.shape[1] == K // block)):
+        if t.dtype != torch.uint8 or not t.is_cuda or not t.is_contiguous() or not shape_ok:
+            raise ValueError("%s: codes must be contiguous uint8 [rows, %d] and scales [rows, %d] "
+                             "on the GPU" % (name, cw, K // block))
+    if codes.shape[0] != scales.shape[0]:
+        raise ValueError("%s: codes and scales disagree on the row count" % name)
+    return codes.shape[0]
+
+
+def mx_matmul_fwd(a_codes, a_scales, b_codes, b_scales, K, block=32, elem="e4m3",
+                  out_dtype=torch.float32, out=None):
+    """H = dec(A) dec(B)^T on the block-scaled matrix cores (Sec. 3.7 eq.
+    (mx-matmul)).  A: MX codes/scales [M, .] along K; B: [N, .].  Returns H
+    [M, N] in out_dtype (float32 or bfloat16)."""
+    if elem not in ELEMS or out_dtype not in OUT_DTYPES:
+        raise ValueError("elem must be 'e4m3' or 'e2m1', out_dtype float32 or bfloat16")
+    M = _mx_operand(a_codes, a_scales, K, block, elem, "A")
+    N = _mx_operand(b_codes, b_scales, K, block, elem, "B")
+    out = _out(out, (M, N), out_dtype, a_codes.device)
+    _check(load().mx_matmul_fwd(_ptr(a_codes), _ptr(a_scales), _ptr(b_codes), _ptr(b_scales),
+                                M, N, K, block, ELEMS[elem], OUT_DTYPES[out_dtype], _ptr(out),
+                                _stream(a_codes.device)))
+    return out
+
+
+def mxnorm_linear_fwd(x, w_codes, w_scales, block=32, elem="e4m3", p=2, coef=0.0, eps=1e-6,
+                      scale_mode="rceil", out_dtype=torch.bfloat16):
+    """The MXNormLinear forward H = MXNorm(X) MXCast(W gamma)^T (Sec. 3.7):
+    MXNorm of the activations, then the MX matmul with a weight cast once by
+    mx_cast_fwd(W, gamma).  Returns (H, rho~)."""
+    codes, scales, rho = mxnorm_mx_fwd(x, block=block, elem=elem, p=p, coef=coef, eps=eps,
+                                       scale_mode=scale_mode)
+    h = mx_matmul_fwd(codes, scales, w_codes, w_scales, x.shape[1], block=block, elem=elem,
+                      out_dtype=out_dtype)
+    return h, rho
 
 
 def mxnorm_default_global_scale(d, block=16, p=2, coef=0.0):

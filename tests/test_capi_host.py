@@ -180,3 +180,21 @@ def test_mx_cast_rejects_bad_arguments():
     assert lib.mx_cast_fwd(None, *ok[1:]) == 1                     # x NULL with T > 0
     assert lib.mx_cast_fwd(*ok[:7], None, *ok[8:]) == 1            # codes NULL
     assert lib.mx_cast_fwd(*ok[:2], -1, *ok[3:]) == 1              # T < 0
+
+
+@pytest.mark.parametrize("args,status", [
+    (dict(M=-1), 1), (dict(K=0), 1), (dict(elem=2), 1), (dict(out_dtype=2), 1),
+    (dict(block=16), 2), (dict(block=64), 2), (dict(K=96), 2), (dict(K=128, elem=1), 2),
+    (dict(N=24), 2), (dict(a=None), 1), (dict(out=None), 1), (dict(a=A8), 1),
+    (dict(bs=OUT + 2), 1), (dict(out=A8), 1), (dict(M=0, a=None, out=None), 0),
+    (dict(N=0, b=None, out=None), 0),
+])
+def test_mx_matmul_rejects_bad_arguments(args, status):
+    lib = mxnorm.load()
+    kw = dict(a=A16, as_=OUT, b=A16, bs=OUT, M=4, N=32, K=256, block=32, elem=0, out_dtype=0,
+              out=OUT)
+    kw.update(args)
+    assert lib.mx_matmul_fwd(kw["a"], kw["as_"], kw["b"], kw["bs"], kw["M"], kw["N"], kw["K"],
+                             kw["block"], kw["elem"], kw["out_dtype"], kw["out"], None) == status
+    if status:
+        assert mxnorm.mx_last_error() != ""

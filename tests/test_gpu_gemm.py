@@ -1,0 +1,171 @@
+"""GPU parity of the MX matrix product (Sec. 3.7 eq. (mx-matmul)) and of the
+MXNormLinear forward against the oracle.
+
+The matrix cores multiply E4M3/E2M1 elements exactly and apply each
+32-element block's E8M0 scales exactly, but accumulate in float32 with their
+own internal alignment: terms far below the largest product of one
+instruction can be dropped.  The test bound is |H - H_oracle| <=
+2^-9 * sum_k |A[m][k] B[n][k]| (plus half a bf16 ulp of H for bf16 output);
+the exactness test below (at most one product per output) pins the operand
+layout and the scale association bit for bit.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2603_13180_amd import mxnorm, synth
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("needs a GPU")
+
+
+def codes_width(K, elem):
+    return K if elem == "e4m3" else K // 2
+
+
+def random_operand(rows, K, elem, rng, smin=117, smax=137):
+    if elem == "e4m3":
+        c = rng.integers(0, 256, (rows, K), dtype=np.uint8)
+        c[(c & 0x7F) == 0x7F] = 0x7E  # no NaN codes
+    else:
+        c = rng.integers(0, 256, (rows, K // 2), dtype=np.uint8)
+    s = rng.integers(smin, smax + 1, (rows, K // 32), dtype=np.uint8)
+    return c, s
+
+
+def abs_codes(c, elem):
+    return c & (0x7F if elem == "e4m3" else 0x77)
+
+
+def gpu_matmul(ac, as_, bc, bs, K, elem, out_dtype=torch.float32):
+    t = [torch.from_numpy(np.ascontiguousarray(v)).to(DEV) for v in (ac, as_, bc, bs)]
+    h = mxnorm.mx_matmul_fwd(*t, K, elem=elem, out_dtype=out_dtype)
+    torch.cuda.synchronize()
+    return h.float().cpu().numpy().astype(np.float64)
+
+
+def assert_close(got, want, mag, bf16, ctx):
+    tol = 2.0 ** -9 * mag + (2.0 ** -8 * np.abs(want) if bf16 else 0.0) + 1e-30
+    same_nan = np.isnan(got) == np.isnan(want)
+    assert same_nan.all(), "%s: NaN pattern differs at %s" % (ctx, np.argwhere(~same_nan)[0])
+    fin = ~np.isnan(want)
+    err = np.abs(got - want)
+    bad = fin & (err > tol)
+    if bad.any():
+        i = tuple(np.argwhere(bad)[0])
+        raise AssertionError("%s: %d outputs off, first %s got %r want %r (sum|ab| %r)" % (
+            ctx, bad.sum(), i, got[i], want[i], mag[i]))
+    ratio = (err[fin] / np.maximum(mag[fin], 1e-300)).max() if fin.any() else 0.0
+    print("%s: max |err| / sum|ab| = %.3g" % (ctx, ratio))
+
+
+ELEMS = ["e4m3", "e2m1"]
+
+
+@pytest.mark.parametrize("elem", ELEMS)
+@pytest.mark.parametrize("M,N,K", [(1, 16, 256), (37, 48, 256), (300, 272, 1024),
+                                   (513, 528, 512), (256, 256, 2048)])
+@pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
+def test_random_operands(elem, M, N, K, out_dtype):
+    rng = np.random.default_rng(M * 7 + N * 3 + K + len(elem))
+    ac, as_ = random_operand(M, K, elem, rng)
+    bc, bs = random_operand(N, K, elem, rng)
+    got = gpu_matmul(ac, as_, bc, bs, K, elem, out_dtype)
+    want = oracle.mx_matmul(ac, as_, bc, bs, K, elem=elem)
+    mag = oracle.mx_matmul(abs_codes(ac, elem), as_, abs_codes(bc, elem), bs, K, elem=elem)
+    assert_close(got, want, mag, out_dtype == torch.bfloat16,
+                 "random %s M=%d N=%d K=%d %s" % (elem, M, N, K, out_dtype))
+
+
+def one_hot_operand(rows, K, elem, pos, rng):
+    """Row r has a single nonzero element, at column pos[r]."""
+    vals = rng.integers(1, 8, rows) if elem == "e2m1" else rng.integers(1, 0x7F, rows)
+    signs = rng.integers(0, 2, rows)
+    if elem == "e4m3":
+        c = np.zeros((rows, K), np.uint8)
+        c[np.arange(rows), pos] = (vals | (signs << 7)).astype(np.uint8)
+    else:
+        c = np.zeros((rows, K // 2), np.uint8)
+        nib = (vals | (signs << 3)).astype(np.uint8)
+        c[np.arange(rows), pos // 2] = np.where(pos % 2 == 1, nib << 4, nib).astype(np.uint8)
+    s = rng.integers(110, 145, (rows, K // 32), dtype=np.uint8)
+    return c, s
+
+
+@pytest.mark.parametrize("elem", ELEMS)
+def test_single_products_are_exact(elem):
+    # every k of a 512-wide K appears; each output is 0 or one product, which
+    # fp32 holds exactly -- a wrong k pairing or scale association shows
+    K = 512
+    M, N = 640, 528
+    rng = np.random.default_rng(5)
+    pa = np.arange(M) % K
+    pb = (np.arange(N) * 7) % K
+    ac, as_ = one_hot_operand(M, K, elem, pa, rng)
+    bc, bs = one_hot_operand(N, K, elem, pb, rng)
+    got = gpu_matmul(ac, as_, bc, bs, K, elem)
+    want = oracle.mx_matmul(ac, as_, bc, bs, K, elem=elem)
+    assert (want != 0).sum() >= M // 8
+    bad = np.argwhere(got != want)
+    assert bad.size == 0, "%d outputs differ, first %s: got %r want %r" % (
+        len(bad), bad[0], got[tuple(bad[0])], want[tuple(bad[0])])
+
+
+@pytest.mark.parametrize("elem", ELEMS)
+def test_nan_scales_and_codes_propagate(elem):
+    K, M, N = 512, 70, 64
+    rng = np.random.default_rng(11)
+    ac, as_ = random_operand(M, K, elem, rng)
+    bc, bs = random_operand(N, K, elem, rng)
+    as_[3, 5] = 0xFF            # NaN scale: row 3 of H is NaN
+    bs[17, 0] = 0xFF            # column 17
+    if elem == "e4m3":
+        ac[40, 300] = 0x7F      # NaN code: row 40
+    got = gpu_matmul(ac, as_, bc, bs, K, elem)
+    want = oracle.mx_matmul(ac, as_, bc, bs, K, elem=elem)
+    assert np.isnan(want[3]).all() and np.isnan(want[:, 17]).all()
+    assert (np.isnan(got) == np.isnan(want)).all()
+    mag = oracle.mx_matmul(abs_codes(ac, elem), as_, abs_codes(bc, elem), bs, K, elem=elem)
+    assert_close(got, want, mag, False, "nan %s" % elem)
+
+
+def test_empty_and_zero_operands():
+    z = torch.empty(0, 256, dtype=torch.uint8, device=DEV)
+    zs = torch.empty(0, 8, dtype=torch.uint8, device=DEV)
+    b = torch.zeros(32, 256, dtype=torch.uint8, device=DEV)
+    bsc = torch.full((32, 8), 127, dtype=torch.uint8, device=DEV)
+    assert mxnorm.mx_matmul_fwd(z, zs, b, bsc, 256).shape == (0, 32)
+    a = torch.zeros(5, 256, dtype=torch.uint8, device=DEV)
+    asc = torch.full((5, 8), 127, dtype=torch.uint8, device=DEV)
+    h = mxnorm.mx_matmul_fwd(a, asc, b, bsc, 256)
+    torch.cuda.synchronize()
+    assert (h == 0).all()
+
+
+@pytest.mark.parametrize("block_elem", [(32, "e4m3"), (32, "e2m1")])
+@pytest.mark.parametrize("T,d,N", [(7, 256, 64), (130, 1024, 272), (257, 2048, 528)])
+def test_mxnorm_linear_forward(block_elem, T, d, N):
+    block, elem = block_elem
+    xb = synth.gaussian(T, d, seed=T + d, scale=1.5)
+    rng = np.random.default_rng(d + N)
+    wb = synth.f32_to_bf16_bits((rng.standard_normal((N, d)) * 0.02).astype(np.float32))
+    gb = synth.f32_to_bf16_bits(rng.uniform(0.5, 1.5, d).astype(np.float32))
+    x = torch.from_numpy(xb.view(np.int16)).to(DEV).view(torch.bfloat16)
+    w = torch.from_numpy(wb.view(np.int16)).to(DEV).view(torch.bfloat16)
+    g = torch.from_numpy(gb.view(np.int16)).to(DEV).view(torch.bfloat16)
+    wc, ws = mxnorm.mx_cast_fwd(w, g, block=block, elem=elem)
+    h, rho = mxnorm.mxnorm_linear_fwd(x, wc, ws, block=block, elem=elem, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    want, ac, as_, r32 = oracle.mxnorm_linear(xb, wb, gb, B=block, elem=elem)
+    assert np.array_equal(rho.cpu().numpy(), r32)
+    wc_o, ws_o = oracle.mxcast_gain(wb, gb, B=block, elem=elem)
+    mag = oracle.mx_matmul(abs_codes(ac, elem), as_, abs_codes(wc_o, elem), ws_o, d, elem=elem)
+    assert_close(h.cpu().numpy().astype(np.float64), want, mag, False,
+                 "mxnorm_linear %s T=%d d=%d N=%d" % (elem, T, d, N))
