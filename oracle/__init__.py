@@ -77,6 +77,8 @@ def _load():
         "mxo_mxnorm_mx": (None, [P, I64, I64, I, I, I, F, F, I, P, P, P, P]),
         "mxo_rmsnorm_mx": (None, [P, P, I64, I64, I, I, F, I, P, P, P, P]),
         "mxo_mxcast_gain": (None, [P, P, I64, I64, I, I, I, P, P]),
+        "mxo_mxcast_t": (ctypes.c_int, [P, P, I64, I64, I, I, I, P, P]),
+        "mxo_ste_bwd": (None, [P, P, P, P, I64, I64, P, P]),
         "mxo_mx_matmul": (ctypes.c_int, [P, P, P, P, I64, I64, I64, I, I, P]),
     }
     for name, (res, args) in sig.items():
@@ -339,3 +341,45 @@ def mxnorm_linear(x, w, gamma=None, B=32, elem="e4m3", p=2, eps=1e-6, mode="rcei
     ac, as_, r32, _ = mxnorm_mx(x, B=B, elem=elem, p=p, eps=eps, mode=mode)
     wc, ws = mxcast_gain(w, gamma, B=B, elem=elem, mode=mode)
     return mx_matmul(ac, as_, wc, ws, x.shape[1], B=B, elem=elem), ac, as_, r32
+
+
+# ------------------------------------------------------ MXNormLinear backward --
+
+def mxcast_t(x, rho=None, B=32, elem="e4m3", mode="rceil"):
+    """Column-wise MX cast of RN32(x * rho) (rho None: x): x bf16 bits [R, C]
+    -> codes [C, R] (E4M3) or [C, R/2] (E2M1), scales [C, R/B] -- the cast
+    along the token dimension the weight gradient needs (Sec. 3.7)."""
+    x = np.ascontiguousarray(x)
+    if x.dtype != np.uint16 or x.ndim != 2:
+        raise TypeError("x must be a 2-D uint16 array of bf16 bit patterns")
+    R, C = x.shape
+    cshape, sshape = _mx_shapes(C, R, B, elem)
+    r = None if rho is None else np.ascontiguousarray(rho, dtype=np.float32)
+    if r is not None and r.shape != (R,):
+        raise ValueError("rho must be float32 [R]")
+    codes = np.empty(cshape, np.uint8)
+    scales = np.empty(sshape, np.uint8)
+    if _load().mxo_mxcast_t(_ptr(x), _ptr(r), R, C, B, ELEMS[elem], SCALE_MODES[mode],
+                            _ptr(codes), _ptr(scales)) != 0:
+        raise MemoryError("mxcast_t: cannot allocate a column buffer")
+    return codes, scales
+
+
+def ste_bwd(x, gz, gamma, rho):
+    """Straight-through-estimator gradients (Sec. 3.7; the RMSNorm-gradient
+    appendix with S = 1/rho~): x, gz bf16 bits [T, d], gamma bf16 bits [d] or
+    None, rho float32 [T].  Returns (grad_x [T, d], grad_gamma [d]) in
+    double."""
+    x = np.ascontiguousarray(x)
+    gz = np.ascontiguousarray(gz)
+    if x.dtype != np.uint16 or gz.dtype != np.uint16 or x.shape != gz.shape or x.ndim != 2:
+        raise TypeError("x and gz must be 2-D uint16 arrays of bf16 bits of one shape")
+    T, d = x.shape
+    g = _as_gamma(gamma, d)
+    r = np.ascontiguousarray(rho, dtype=np.float32)
+    if r.shape != (T,):
+        raise ValueError("rho must be float32 [T]")
+    gx = np.empty((T, d), np.float64)
+    gg = np.empty(d, np.float64)
+    _load().mxo_ste_bwd(_ptr(x), _ptr(gz), _ptr(g), _ptr(r), T, d, _ptr(gx), _ptr(gg))
+    return gx, gg

@@ -56,6 +56,20 @@
  *       v = RN32(t / den); code = E2M1(v); if dec(S) == 0 every code of the
  *       block is a signed zero.
  *
+ *
+ * Parity unpinned: the paper prints no value that fixes readings R3 (the
+ * value and place of epsilon), R8 (the non-finite policy), R9 (the NVFP4
+ * conventions: s_g, nibble order, division order) and FLOOR mode's
+ * saturation (R4).  The functions that carry them are checked against their
+ * written definitions and the invariants above, not against a value from the
+ * paper.
+ *
+ * Also here, for the MXNormLinear layer (Sec. 3.7; the implementation
+ * appendix's mx_norm_linear_forward/backward and the RMSNorm-gradient
+ * appendix): the gain-folded weight cast, the MX matmul, the column-wise
+ * (transposing) MX cast of the backward pass, and the straight-through
+ * estimator of the gradients.
+ *
  * Build: gcc -O2 -fPIC -shared -ffp-contract=off -fno-fast-math -o ... -lm
  * (no FMA contraction, no flush-to-zero; x86-64 SSE arithmetic is IEEE
  * binary32/binary64 with round-to-nearest-even).
@@ -697,4 +711,83 @@ int mxo_mx_matmul(const uint8_t *a_codes, const uint8_t *a_scales, const uint8_t
     }
     free(db);
     return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* MXNormLinear backward (Sec. 3.7; the RMSNorm-gradient appendix; the        */
+/* implementation appendix's mx_norm_linear_backward)                        */
+/* ------------------------------------------------------------------------ */
+
+/* Column-wise MX cast: y = RN32(x * rho) (rho NULL: y = x), then the plain MX
+ * cast of y^T, i.e. blocks of B consecutive rows of one column.  This is the
+ * quantisation "along columns" the weight gradient needs: MXCast(rho~ . X)
+ * and MXCast(grad_H^T) are blocked along the token dimension.
+ * x: bf16 bits [R, C]; rho: float [R] or NULL; codes: [C, R] (E4M3) or
+ * [C, R/2] (E2M1); scales: [C, R/B].  NaN blocks take their codes' signs from
+ * x (R8).  Returns 0, or -1 if a column buffer cannot be allocated. */
+int mxo_mxcast_t(const uint16_t *x, const float *rho, int64_t R, int64_t C, int B, int elem,
+                 int mode, uint8_t *codes, uint8_t *scales)
+{
+    int64_t c, i, k, K = R / B;
+    float *y = malloc(sizeof(float) * (size_t)R);
+    uint16_t *sgn = malloc(sizeof(uint16_t) * (size_t)R);
+    uint8_t *colcodes = malloc((size_t)R);
+    if (!y || !sgn || !colcodes) {
+        free(y);
+        free(sgn);
+        free(colcodes);
+        return -1;
+    }
+    for (c = 0; c < C; c++) {
+        for (i = 0; i < R; i++) {
+            sgn[i] = x[i * C + c];
+            y[i] = mxo_bf16_to_float(sgn[i]);
+            if (rho)
+                y[i] = y[i] * rho[i];
+        }
+        for (k = 0; k < K; k++)
+            scales[c * K + k] = mx_cast_block(y + k * B, sgn + k * B, B, mode, elem,
+                                              colcodes + k * B);
+        store_row_codes(colcodes, R, elem, codes + c * (elem == MXO_ELEM_E2M1 ? R / 2 : R));
+    }
+    free(y);
+    free(sgn);
+    free(colcodes);
+    return 0;
+}
+
+/* The straight-through estimator (Sec. 3.7: RMSNorm's gradient with the RMS
+ * S replaced by the MXNorm estimate 1/rho~), written out from the
+ * RMSNorm-gradient appendix for one row t of X [T, d]:
+ *   dXb_j = gz_j gamma_j                      (grad of X-bar = grad_Z gamma)
+ *   u     = sum_j dXb_j x_j
+ *   gx_j  = rho dXb_j - (1/d) rho^3 u x_j     (S^-1 = rho, S^-3 = rho^3)
+ *   ggamma_j += (rho x_j) gz_j                (sum over rows of X-bar grad_Z)
+ * gz is grad_Z = grad_Y W, the gradient at the normalised, gained output.
+ * Everything in double from the bf16 inputs and the float rho; gamma NULL
+ * means gamma = 1; ggamma may be NULL. */
+void mxo_ste_bwd(const uint16_t *x, const uint16_t *gz, const uint16_t *gamma, const float *rho,
+                 int64_t T, int64_t d, double *gx, double *ggamma)
+{
+    int64_t t, j;
+    if (ggamma)
+        for (j = 0; j < d; j++)
+            ggamma[j] = 0.0;
+    for (t = 0; t < T; t++) {
+        const double r = (double)rho[t];
+        double u = 0.0;
+        for (j = 0; j < d; j++) {
+            const double g = gamma ? (double)mxo_bf16_to_float(gamma[j]) : 1.0;
+            u += (double)mxo_bf16_to_float(gz[t * d + j]) * g *
+                 (double)mxo_bf16_to_float(x[t * d + j]);
+        }
+        for (j = 0; j < d; j++) {
+            const double g = gamma ? (double)mxo_bf16_to_float(gamma[j]) : 1.0;
+            const double xj = (double)mxo_bf16_to_float(x[t * d + j]);
+            const double dxb = (double)mxo_bf16_to_float(gz[t * d + j]) * g;
+            gx[t * d + j] = r * dxb - r * r * r * u * xj / (double)d;
+            if (ggamma)
+                ggamma[j] += r * xj * (double)mxo_bf16_to_float(gz[t * d + j]);
+        }
+    }
 }
