@@ -46,6 +46,7 @@
 #ifndef MXNORM_H
 #define MXNORM_H
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
@@ -181,7 +182,51 @@ typedef enum {
  */
 mx_status mx_matmul_fwd(const uint8_t *a_codes, const uint8_t *a_scales, const uint8_t *b_codes,
                         const uint8_t *b_scales, int64_t M, int64_t N, int64_t K, int block,
-                        int elem, int out_dtype, void *out, void *stream);
+                        int elem, const void *b_gain, int out_dtype, void *out, void *stream);
+/* b_gain: bf16 [N] or NULL.  When given, H[m][n] = RN(acc * b_gain[n]) in
+ * float: the gain applied after the product, as the weight gradient needs
+ * (Sec. 3.7: grad W = MXCast(grad_H^T) MXCast(rho~ . X) . gamma); 8-byte
+ * aligned. */
+
+/*
+ * Column-wise MX cast for the MXNormLinear backward (Sec. 3.7): y =
+ * RN(x * rho[r]) in float (rho NULL: y = x), then the MX encoding of y^T,
+ * blocked along the rows of x.  x: bf16 [R, C] row-major (device); rho: float
+ * [R] or NULL; codes: [C, R] (E4M3) or [C, R/2] (E2M1, two per byte, element
+ * 2j in the low nibble); scales: E8M0 [C, R/32].  Scale rule, rounding and
+ * the NaN-block codes as in the forward entry points (signs from x).  With x
+ * = X and rho = rho~ this is MXCast(rho~ . X) blocked along tokens; with rho
+ * NULL it gives MXCast(grad_H^T) and the weight blocked along its output
+ * dimension.  block: 32 (else MX_EUNSUPPORTED).  R a multiple of 32 and C of
+ * 8 (else MX_EINVAL); x and codes 16-byte aligned, rho 4-byte.  R == 0 is a
+ * no-op.
+ */
+mx_status mx_cast_t_fwd(const void *x, const float *rho, int64_t R, int64_t C, int block,
+                        int elem, int scale_mode, uint8_t *codes, uint8_t *scales, void *stream);
+
+/*
+ * The straight-through estimator of the MXNorm backward (Sec. 3.7: RMSNorm's
+ * gradient used for MXNorm; the RMSNorm-gradient appendix with the RMS S
+ * replaced by the estimate 1/rho~).  Per row t of x [T, d]:
+ *   dXb = grad_z * gamma;  u = sum_j dXb_j x_j;
+ *   grad_x_j = rho dXb_j - (1/d) rho^3 u x_j;
+ *   grad_gamma_j = sum_t (rho_t x_tj) grad_z_tj.
+ * x, grad_z: bf16 [T, d] (grad_z is the gradient at the norm's gained
+ * output, grad_Y W); gamma: bf16 [d] or NULL (= 1); rho: float [T], the rho~
+ * the forward returned.  grad_x: [T, d] float32 or bf16 (out_dtype).
+ * Arithmetic: dXb exact in float, u summed in double, c = rho^3 u / d in
+ * double rounded to float, grad_x = RN(RN(rho dXb) - RN(c x)); the
+ * grad_gamma partial sums are float over 32 rows, then summed in double in a
+ * fixed order (deterministic).  grad_gamma: float [d] or NULL (not computed);
+ * it needs `workspace`, caller-owned device memory of at least
+ * mxnorm_ste_bwd_workspace_bytes(T, d) bytes (16-byte aligned), overwritten.
+ * d a multiple of 8 and <= MXNORM_MAX_D; 16-byte alignment of x, grad_z,
+ * gamma, grad_x; T == 0 is a no-op.
+ */
+size_t mxnorm_ste_bwd_workspace_bytes(int64_t T, int64_t d);
+mx_status mxnorm_ste_bwd(const void *x, const void *grad_z, const void *gamma, const float *rho,
+                         int64_t T, int64_t d, int out_dtype, void *grad_x, float *grad_gamma,
+                         void *workspace, size_t workspace_bytes, void *stream);
 
 /*
  * Default NVFP4 tensor decode scales: an output bound divided by 6 * 448, so

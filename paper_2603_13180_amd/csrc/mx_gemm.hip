@@ -52,6 +52,7 @@ template <int ELEM> struct Op {
 
 struct Args {
     const uint8_t *a, *as, *b, *bs;
+    const uint16_t *bgain; // bf16 [N] or NULL
     void *out;
     int64_t M, N;
     int64_t rb;   // code bytes per row
@@ -368,7 +369,14 @@ __global__ void __launch_bounds__(NT) mx_gemm_kernel(Args A)
             const int64_t n = n0 + wn + 16 * i + 4 * g;
             if (n >= A.N)
                 continue;
-            const v4f v = acc[i][j];
+            v4f v = acc[i][j];
+            if (A.bgain) {
+                const uint2 gw = *reinterpret_cast<const uint2 *>(A.bgain + n);
+                v[0] = v[0] * __uint_as_float(gw.x << 16);
+                v[1] = v[1] * __uint_as_float(gw.x & 0xFFFF0000u);
+                v[2] = v[2] * __uint_as_float(gw.y << 16);
+                v[3] = v[3] * __uint_as_float(gw.y & 0xFFFF0000u);
+            }
             if constexpr (OUT == MX_OUT_F32) {
                 *reinterpret_cast<float4 *>(static_cast<float *>(A.out) + m * A.N + n) =
                     make_float4(v[0], v[1], v[2], v[3]);
@@ -404,7 +412,7 @@ extern "C" {
 
 mx_status mx_matmul_fwd(const uint8_t *a_codes, const uint8_t *a_scales, const uint8_t *b_codes,
                         const uint8_t *b_scales, int64_t M, int64_t N, int64_t K, int block,
-                        int elem, int out_dtype, void *out, void *stream)
+                        int elem, const void *b_gain, int out_dtype, void *out, void *stream)
 {
     mxk::clear_error();
     if (M < 0 || N < 0 || K <= 0)
@@ -427,9 +435,10 @@ mx_status mx_matmul_fwd(const uint8_t *a_codes, const uint8_t *a_scales, const u
     if (!a_codes || !a_scales || !b_codes || !b_scales || !out)
         return mxk::fail(MX_EINVAL, "NULL pointer");
     if (!aligned(a_codes, 16) || !aligned(b_codes, 16) || !aligned(a_scales, 4) ||
-        !aligned(b_scales, 4) || !aligned(out, out_dtype == MX_OUT_F32 ? 16 : 8))
-        return mxk::fail(MX_EINVAL, "codes must be 16-byte, scales 4-byte and out 16-byte (f32) or "
-                               "8-byte (bf16) aligned");
+        !aligned(b_scales, 4) || !aligned(out, out_dtype == MX_OUT_F32 ? 16 : 8) ||
+        (b_gain && !aligned(b_gain, 8)))
+        return mxk::fail(MX_EINVAL, "codes must be 16-byte, scales 4-byte, out 16-byte (f32) or "
+                               "8-byte (bf16) and b_gain 8-byte aligned");
     const int64_t tm = (M + mxg::BM - 1) / mxg::BM, tn = (N + mxg::BN - 1) / mxg::BN;
     if (tm * tn > INT32_MAX / 2 || M > INT32_MAX || N > INT32_MAX)
         return mxk::fail(MX_EUNSUPPORTED, "problem too large");
@@ -438,6 +447,7 @@ mx_status mx_matmul_fwd(const uint8_t *a_codes, const uint8_t *a_scales, const u
     A.as = a_scales;
     A.b = b_codes;
     A.bs = b_scales;
+    A.bgain = static_cast<const uint16_t *>(b_gain);
     A.out = out;
     A.M = M;
     A.N = N;

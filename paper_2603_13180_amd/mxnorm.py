@@ -52,7 +52,10 @@ def load():
         "mxnorm_mx_fwd": (I, [P, I64, I64, I, I, I, F, F, I, P, P, P, P]),
         "rmsnorm_mx_fwd": (I, [P, P, I64, I64, I, I, F, I, P, P, P, P]),
         "mx_cast_fwd": (I, [P, P, I64, I64, I, I, I, P, P, P]),
-        "mx_matmul_fwd": (I, [P, P, P, P, I64, I64, I64, I, I, I, P, P]),
+        "mx_matmul_fwd": (I, [P, P, P, P, I64, I64, I64, I, I, P, I, P, P]),
+        "mx_cast_t_fwd": (I, [P, P, I64, I64, I, I, I, P, P, P]),
+        "mxnorm_ste_bwd_workspace_bytes": (ctypes.c_size_t, [I64, I64]),
+        "mxnorm_ste_bwd": (I, [P, P, P, P, I64, I64, I, P, P, P, ctypes.c_size_t, P]),
         "mxnorm_default_global_scale": (F, [I64, I, I, F]),
         "rmsnorm_default_global_scale": (F, [I64, F]),
         "mxnorm_coef": (F, [I, I]),
@@ -246,18 +249,22 @@ def _mx_operand(codes, scales, K, block, elem, name):
 
 
 def mx_matmul_fwd(a_codes, a_scales, b_codes, b_scales, K, block=32, elem="e4m3",
-                  out_dtype=torch.float32, out=None):
+                  out_dtype=torch.float32, out=None, b_gain=None):
     """H = dec(A) dec(B)^T on the block-scaled matrix cores (Sec. 3.7 eq.
-    (mx-matmul)).  A: MX codes/scales [M, .] along K; B: [N, .].  Returns H
-    [M, N] in out_dtype (float32 or bfloat16)."""
+    (mx-matmul)).  A: MX codes/scales [M, .] along K; B: [N, .].  b_gain
+    (bf16 [N]) multiplies column n of H after the product.  Returns H [M, N]
+    in out_dtype (float32 or bfloat16)."""
     if elem not in ELEMS or out_dtype not in OUT_DTYPES:
         raise ValueError("elem must be 'e4m3' or 'e2m1', out_dtype float32 or bfloat16")
     M = _mx_operand(a_codes, a_scales, K, block, elem, "A")
     N = _mx_operand(b_codes, b_scales, K, block, elem, "B")
+    if b_gain is not None and (b_gain.dtype != torch.bfloat16 or b_gain.shape != (N,) or
+                               b_gain.device != a_codes.device or not b_gain.is_contiguous()):
+        raise ValueError("b_gain must be a contiguous bfloat16 [N] tensor on the GPU")
     out = _out(out, (M, N), out_dtype, a_codes.device)
     _check(load().mx_matmul_fwd(_ptr(a_codes), _ptr(a_scales), _ptr(b_codes), _ptr(b_scales),
-                                M, N, K, block, ELEMS[elem], OUT_DTYPES[out_dtype], _ptr(out),
-                                _stream(a_codes.device)))
+                                M, N, K, block, ELEMS[elem], _ptr(b_gain),
+                                OUT_DTYPES[out_dtype], _ptr(out), _stream(a_codes.device)))
     return out
 
 
@@ -271,6 +278,85 @@ def mxnorm_linear_fwd(x, w_codes, w_scales, block=32, elem="e4m3", p=2, coef=0.0
     h = mx_matmul_fwd(codes, scales, w_codes, w_scales, x.shape[1], block=block, elem=elem,
                       out_dtype=out_dtype)
     return h, rho
+
+
+def mx_cast_t_fwd(x, rho=None, block=32, elem="e4m3", scale_mode="rceil", codes=None,
+                  scales=None):
+    """Column-wise MX cast (Sec. 3.7): the MX encoding of (rho[:, None] * x)^T,
+    blocked along x's rows.  x bf16 [R, C] -> codes [C, R] (E4M3) or
+    [C, R/2] (E2M1), scales [C, R/32]."""
+    R, C = _input(x)
+    if rho is not None and (rho.dtype != torch.float32 or rho.shape != (R,) or
+                            rho.device != x.device or not rho.is_contiguous()):
+        raise ValueError("rho must be a contiguous float32 [R] tensor on x's device")
+    if elem not in ELEMS:
+        raise ValueError("elem must be 'e4m3' or 'e2m1'")
+    codes = _out(codes, (C, R) if elem == "e4m3" else (C, R // 2), torch.uint8, x.device)
+    scales = _out(scales, (C, R // block), torch.uint8, x.device)
+    _check(load().mx_cast_t_fwd(_ptr(x), _ptr(rho), R, C, block, ELEMS[elem],
+                                SCALE_MODES[scale_mode], _ptr(codes), _ptr(scales),
+                                _stream(x.device)))
+    return codes, scales
+
+
+def mxnorm_ste_bwd(x, grad_z, gamma, rho, out_dtype=torch.bfloat16, want_grad_gamma=True,
+                   grad_x=None, grad_gamma=None, workspace=None):
+    """The straight-through estimator of the MXNorm backward (Sec. 3.7; the
+    RMSNorm-gradient appendix with S = 1/rho~).  x, grad_z bf16 [T, d];
+    gamma bf16 [d] or None; rho float32 [T] from the forward.  Returns
+    (grad_x [T, d] in out_dtype, grad_gamma float32 [d] or None)."""
+    T, d = _input(x)
+    if grad_z.dtype != torch.bfloat16 or grad_z.shape != x.shape or grad_z.device != x.device \
+            or not grad_z.is_contiguous():
+        raise ValueError("grad_z must be a contiguous bfloat16 tensor shaped like x")
+    g = _gamma(gamma, x)
+    if rho.dtype != torch.float32 or rho.shape != (T,) or rho.device != x.device:
+        raise ValueError("rho must be float32 [T] on x's device")
+    if out_dtype not in OUT_DTYPES:
+        raise ValueError("out_dtype must be float32 or bfloat16")
+    lib = load()
+    grad_x = _out(grad_x, (T, d), out_dtype, x.device)
+    ws_bytes = 0
+    if want_grad_gamma:
+        grad_gamma = _out(grad_gamma, (d,), torch.float32, x.device)
+        ws_bytes = int(lib.mxnorm_ste_bwd_workspace_bytes(T, d))
+        if workspace is None:
+            workspace = torch.empty(max(ws_bytes, 16), dtype=torch.uint8, device=x.device)
+        elif workspace.numel() * workspace.element_size() < ws_bytes:
+            raise ValueError("workspace smaller than mxnorm_ste_bwd_workspace_bytes(T, d)")
+        ws_bytes = workspace.numel() * workspace.element_size()
+    _check(lib.mxnorm_ste_bwd(_ptr(x), _ptr(grad_z), _ptr(g), _ptr(rho.contiguous()), T, d,
+                              OUT_DTYPES[out_dtype], _ptr(grad_x),
+                              _ptr(grad_gamma) if want_grad_gamma else None,
+                              _ptr(workspace) if want_grad_gamma else None, ws_bytes,
+                              _stream(x.device)))
+    return grad_x, (grad_gamma if want_grad_gamma else None)
+
+
+def mxnorm_linear_bwd(grad_h, x, rho, gamma, w, block=32, elem="e4m3",
+                      grad_x_dtype=torch.bfloat16):
+    """The MXNormLinear backward (Sec. 3.7; the implementation appendix's
+    mx_norm_linear_backward), every product and cast in the library:
+      grad_Z = MXCast(grad_H) MXCast_N(W)            (W blocked along N)
+      grad_X, grad_gamma = STE(X, grad_Z, gamma, rho~)
+      grad_W = (MXCast(grad_H^T) MXCast(rho~ X)^T) . gamma
+    grad_h bf16 [T, N], x bf16 [T, d], rho float32 [T], gamma bf16 [d],
+    w bf16 [N, d].  Returns (grad_x, grad_gamma float32 [d], grad_w float32
+    [N, d])."""
+    T, N = grad_h.shape
+    d = x.shape[1]
+    if w.shape != (N, d):
+        raise ValueError("w must be [N, d]")
+    gh_c, gh_s = mx_cast_fwd(grad_h, None, block=block, elem=elem)
+    wt_c, wt_s = mx_cast_t_fwd(w, None, block=block, elem=elem)
+    grad_z = mx_matmul_fwd(gh_c, gh_s, wt_c, wt_s, N, block=block, elem=elem,
+                           out_dtype=torch.bfloat16)
+    grad_x, grad_gamma = mxnorm_ste_bwd(x, grad_z, gamma, rho, out_dtype=grad_x_dtype)
+    ght_c, ght_s = mx_cast_t_fwd(grad_h, None, block=block, elem=elem)
+    xt_c, xt_s = mx_cast_t_fwd(x, rho, block=block, elem=elem)
+    grad_w = mx_matmul_fwd(ght_c, ght_s, xt_c, xt_s, T, block=block, elem=elem,
+                           out_dtype=torch.float32, b_gain=gamma)
+    return grad_x, grad_gamma, grad_w
 
 
 def mxnorm_default_global_scale(d, block=16, p=2, coef=0.0):

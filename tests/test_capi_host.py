@@ -187,14 +187,51 @@ def test_mx_cast_rejects_bad_arguments():
     (dict(block=16), 2), (dict(block=64), 2), (dict(K=96), 2), (dict(K=128, elem=1), 2),
     (dict(N=24), 2), (dict(a=None), 1), (dict(out=None), 1), (dict(a=A8), 1),
     (dict(bs=OUT + 2), 1), (dict(out=A8), 1), (dict(M=0, a=None, out=None), 0),
-    (dict(N=0, b=None, out=None), 0),
+    (dict(N=0, b=None, out=None), 0), (dict(gain=OUT + 4), 1), (dict(K=1 << 23), 2),
 ])
 def test_mx_matmul_rejects_bad_arguments(args, status):
     lib = mxnorm.load()
-    kw = dict(a=A16, as_=OUT, b=A16, bs=OUT, M=4, N=32, K=256, block=32, elem=0, out_dtype=0,
-              out=OUT)
+    kw = dict(a=A16, as_=OUT, b=A16, bs=OUT, M=4, N=32, K=256, block=32, elem=0, gain=None,
+              out_dtype=0, out=OUT)
     kw.update(args)
     assert lib.mx_matmul_fwd(kw["a"], kw["as_"], kw["b"], kw["bs"], kw["M"], kw["N"], kw["K"],
-                             kw["block"], kw["elem"], kw["out_dtype"], kw["out"], None) == status
+                             kw["block"], kw["elem"], kw["gain"], kw["out_dtype"], kw["out"],
+                             None) == status
     if status:
         assert mxnorm.mx_last_error() != ""
+
+
+@pytest.mark.parametrize("args,status", [
+    (dict(R=-1), 1), (dict(C=0), 1), (dict(elem=2), 1), (dict(mode=3), 1), (dict(block=16), 2),
+    (dict(R=48), 1), (dict(C=12), 1), (dict(x=None), 1), (dict(codes=None), 1), (dict(x=A8), 1),
+    (dict(rho=OUT + 2), 1), (dict(R=0, x=None, codes=None, scales=None), 0),
+])
+def test_mx_cast_t_rejects_bad_arguments(args, status):
+    lib = mxnorm.load()
+    kw = dict(x=A16, rho=None, R=64, C=16, block=32, elem=0, mode=0, codes=OUT, scales=OUT)
+    kw.update(args)
+    assert lib.mx_cast_t_fwd(kw["x"], kw["rho"], kw["R"], kw["C"], kw["block"], kw["elem"],
+                             kw["mode"], kw["codes"], kw["scales"], None) == status
+
+
+def test_ste_workspace_size():
+    lib = mxnorm.load()
+    assert lib.mxnorm_ste_bwd_workspace_bytes(0, 4096) == 0
+    assert lib.mxnorm_ste_bwd_workspace_bytes(1, 4096) == 4096 * 4
+    assert lib.mxnorm_ste_bwd_workspace_bytes(32, 4096) == 4096 * 4
+    assert lib.mxnorm_ste_bwd_workspace_bytes(33, 4096) == 2 * 4096 * 4
+
+
+@pytest.mark.parametrize("args,status", [
+    (dict(T=-1), 1), (dict(d=0), 1), (dict(d=12), 1), (dict(d=65536), 2), (dict(out=2), 1),
+    (dict(x=None), 1), (dict(rho=None), 1), (dict(gx=None), 1), (dict(x=A8), 1),
+    (dict(gamma=A8), 1), (dict(gg=OUT, ws=None), 1), (dict(gg=OUT, ws=OUT, wsb=16), 1),
+    (dict(gg=OUT + 2), 1), (dict(T=0, x=None, gz=None, rho=None, gx=None), 0),
+])
+def test_ste_rejects_bad_arguments(args, status):
+    lib = mxnorm.load()
+    kw = dict(x=A16, gz=A16, gamma=None, rho=OUT, T=4, d=64, out=1, gx=OUT, gg=None, ws=None,
+              wsb=0)
+    kw.update(args)
+    assert lib.mxnorm_ste_bwd(kw["x"], kw["gz"], kw["gamma"], kw["rho"], kw["T"], kw["d"],
+                              kw["out"], kw["gx"], kw["gg"], kw["ws"], kw["wsb"], None) == status
