@@ -27,7 +27,9 @@ PEAK_HBM_GBPS = 8000.0
 WORKLOAD = "llama3-8b-d4096"
 NV_WORKLOAD = "llama3-8b-d4096-nvfp4"
 ROTATE_MIN_BYTES = 768 << 20       # > 3x the 256 MiB Infinity Cache
-KERNEL_SRC = os.path.join(ROOT, "paper_2603_13180_amd", "csrc", "mxnorm.hip")
+# the norm/cast kernel body and its launch configuration
+KERNEL_SRC = [os.path.join(ROOT, "paper_2603_13180_amd", "csrc", f)
+              for f in ("norm_cast.h", "mxnorm.hip")]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_mxnorm_mxfp8_llama3-8b-d4096.txt")
 
 
@@ -43,6 +45,9 @@ def parse():
     ap.add_argument("--layer", metavar="OUT_JSON",
                     help="instead of the headline line, run the MXNormLinear layer benchmark "
                          "(norm + MX matmul at Llama-3-8B projection shapes) and write results")
+    ap.add_argument("--backward", metavar="OUT_JSON",
+                    help="instead of the headline line, time the MXNormLinear backward "
+                         "(casts, STE, both matmuls) at Llama-3-8B projection shapes")
     ap.add_argument("--sweep-formats",
                     default="e4m3-b32,nvfp4,e4m3-b16,e4m3-b64,e2m1-b16,e2m1-b32,e2m1-b64",
                     help="comma list of e4m3-b{16,32,64}, e2m1-b{16,32,64}, nvfp4")
@@ -271,6 +276,109 @@ def run_layer(path):
     print(json.dumps({"layer": path, "summary": summary}))
 
 
+def ste_bytes(T, d):
+    """Algorithmic bytes of one STE launch: x, grad_Z read and grad_x (bf16)
+    written per element, rho per row, gamma read and grad_gamma written once."""
+    return T * d * 6 + 4 * T + 2 * d + 4 * d
+
+
+def cast_t_bytes(T, d):
+    """Algorithmic bytes of the column cast of rho~ X to MXFP8."""
+    return T * d * 2 + T * d + T * d // 32 + 4 * T
+
+
+def backward_case(fmt, T, N, stream, gen, rounds=3, budget_ms=40.0):
+    """The MXNormLinear backward at one shape: every stage captured alone and
+    the whole chain captured as one graph, medians of interleaved rounds."""
+    import numpy as np
+    import torch
+    from paper_2603_13180_amd import mxnorm
+
+    dev = torch.device("cuda:0")
+    d = LAYER_D
+    x = torch.randn(T, d, generator=gen, device=dev).to(torch.bfloat16)
+    w = (0.02 * torch.randn(N, d, generator=gen, device=dev)).to(torch.bfloat16)
+    gam = (1.0 + 0.1 * torch.randn(d, generator=gen, device=dev)).to(torch.bfloat16)
+    gh = (0.01 * torch.randn(T, N, generator=gen, device=dev)).to(torch.bfloat16)
+    _, _, rho = mxnorm.mxnorm_mx_fwd(x, 32, fmt)
+    cw = lambda n: n if fmt == "e4m3" else n // 2
+    u8 = lambda *shape: torch.empty(*shape, dtype=torch.uint8, device=dev)
+    gh_c, gh_s = u8(T, cw(N)), u8(T, N // 32)
+    wt_c, wt_s = u8(d, cw(N)), u8(d, N // 32)
+    ght_c, ght_s = u8(N, cw(T)), u8(N, T // 32)
+    xt_c, xt_s = u8(d, cw(T)), u8(d, T // 32)
+    gz = torch.empty(T, d, dtype=torch.bfloat16, device=dev)
+    gx = torch.empty(T, d, dtype=torch.bfloat16, device=dev)
+    gg = torch.empty(d, dtype=torch.float32, device=dev)
+    gw = torch.empty(N, d, dtype=torch.float32, device=dev)
+    ws = u8(max(16, mxnorm.load().mxnorm_ste_bwd_workspace_bytes(T, d)))
+
+    stages = {
+        "cast_grad_h": lambda _: mxnorm.mx_cast_fwd(gh, None, 32, fmt, codes=gh_c, scales=gh_s),
+        "cast_t_w": lambda _: mxnorm.mx_cast_t_fwd(w, None, 32, fmt, codes=wt_c, scales=wt_s),
+        "matmul_grad_z": lambda _: mxnorm.mx_matmul_fwd(gh_c, gh_s, wt_c, wt_s, N, elem=fmt,
+                                                        out_dtype=torch.bfloat16, out=gz),
+        "ste": lambda _: mxnorm.mxnorm_ste_bwd(x, gz, gam, rho, grad_x=gx, grad_gamma=gg,
+                                               workspace=ws),
+        "cast_t_grad_h": lambda _: mxnorm.mx_cast_t_fwd(gh, None, 32, fmt, codes=ght_c,
+                                                        scales=ght_s),
+        "cast_t_rho_x": lambda _: mxnorm.mx_cast_t_fwd(x, rho, 32, fmt, codes=xt_c,
+                                                       scales=xt_s),
+        "matmul_grad_w": lambda _: mxnorm.mx_matmul_fwd(ght_c, ght_s, xt_c, xt_s, T, elem=fmt,
+                                                        out_dtype=torch.float32, out=gw,
+                                                        b_gain=gam),
+    }
+
+    def whole(i):
+        for f in stages.values():
+            f(i)
+
+    flops = 2.0 * 2 * T * N * d
+    reps = max(2, int(budget_ms / (flops / 1.5e15 * 1e3)))
+    t = {k: [] for k in list(stages) + ["backward"]}
+    for _ in range(rounds):
+        t["backward"].append(graph_time(whole, 1, reps, 1, stream))
+        for k, f in stages.items():
+            t[k].append(graph_time(f, 1, reps, 1, stream))
+    m = {k: float(np.median(v)) for k, v in t.items()}
+    out = {"format": fmt, "tokens": T, "N": N, "d": d,
+           "backward_us": round(m["backward"] * 1e3, 2),
+           "stages_us": {k: round(m[k] * 1e3, 2) for k in stages},
+           "matmul_TFLOPs": {k: round(2.0 * T * N * d / (m[k] * 1e-3) / 1e12, 1)
+                             for k in ("matmul_grad_z", "matmul_grad_w")},
+           "ste_GBps": round(ste_bytes(T, d) / (m["ste"] * 1e-3) / 1e9, 1),
+           "cast_t_rho_x_GBps": round((T * d * 2 + T * cw(d) + T * d // 32 + 4 * T)
+                                      / (m["cast_t_rho_x"] * 1e-3) / 1e9, 1)}
+    del x, w, gh, gz, gx, gw, ws
+    torch.cuda.empty_cache()
+    return out
+
+
+def run_backward(path):
+    import torch
+    from paper_2603_13180_amd import mxnorm
+    mxnorm.load()
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.Stream(dev)
+    gen = torch.Generator(device=dev)
+    results = []
+    for fmt in ("e4m3", "e2m1"):
+        for name, N in LAYER_N.items():
+            for T in (4096, 16384, 32768):
+                gen.manual_seed(T + N)
+                r = backward_case(fmt, T, N, stream, gen)
+                r["projection"] = name
+                results.append(r)
+                print(json.dumps(r), file=sys.stderr, flush=True)
+    doc = {"method": "each stage and the whole chain captured as HIP graphs, replayed ~40 ms "
+                     "per round, median of 3 interleaved rounds; N(0,1) activations, "
+                     "0.02 N(0,1) weights, 0.01 N(0,1) output gradients",
+           "results": results}
+    with open(path, "w") as f:
+        json.dump(doc, f, indent=1)
+    print(json.dumps({"backward": path, "shapes": len(results)}))
+
+
 def mxfp8_bytes(T, d):
     return T * d * 2 + T * d + T * (d // 32) + 4 * T
 
@@ -280,7 +388,10 @@ def nvfp4_bytes(T, d):
 
 
 def source_hash():
-    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for f in KERNEL_SRC:
+        h.update(open(f, "rb").read())
+    return h.hexdigest()[:16]
 
 
 def measured_traffic():
@@ -346,6 +457,9 @@ def main():
         return
     if args.layer:
         run_layer(args.layer)
+        return
+    if args.backward:
+        run_backward(args.backward)
         return
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
@@ -438,6 +552,28 @@ def main():
     m = time_launches(lambda i: dst.copy_(xs[i]), n_sets, 50, 5, stream)
     copy_gbps = 2 * x0.numel() * 2 / (m * 1e-3) / 1e9
 
+    # the backward's streaming kernels at the same shape: the STE (x and a
+    # synthetic grad_Z in rotation) and the column cast of rho~ X
+    gzs = [torch.randn(T, d, device=dev).to(torch.bfloat16) for _ in range(n_sets)]
+    gxo = torch.empty(T, d, dtype=torch.bfloat16, device=dev)
+    ggo = torch.empty(d, dtype=torch.float32, device=dev)
+    wsp = torch.empty(mxnorm.load().mxnorm_ste_bwd_workspace_bytes(T, d), dtype=torch.uint8,
+                      device=dev)
+    tc = torch.empty(d, T, dtype=torch.uint8, device=dev)
+    ts = torch.empty(d, T // 32, dtype=torch.uint8, device=dev)
+    ms_ste = time_launches(lambda i: mxnorm.mxnorm_ste_bwd(
+        xs[i], gzs[i], g, rho[i], grad_x=gxo, grad_gamma=ggo, workspace=wsp),
+        n_sets, 50, 5, stream)
+    ms_ct = time_launches(lambda i: mxnorm.mx_cast_t_fwd(xs[i], rho[i], codes=tc, scales=ts),
+                          n_sets, 50, 5, stream)
+    bwd = {"ste_bwd": {"us": round(ms_ste * 1e3, 2),
+                       "GB/s": round(ste_bytes(T, d) / (ms_ste * 1e-3) / 1e9, 1)},
+           "cast_t_rho_x_mxfp8": {"us": round(ms_ct * 1e3, 2),
+                                  "GB/s": round(cast_t_bytes(T, d) / (ms_ct * 1e-3) / 1e9, 1)}}
+    for v in bwd.values():
+        v["pct_of_peak"] = round(100 * v["GB/s"] / PEAK_HBM_GBPS, 2)
+    del gzs, gxo, wsp, tc, ts
+
     # the MX matmul the MXNorm output feeds (Llama-3-8B QKV projection)
     del ncodes, nscales, small
     torch.cuda.empty_cache()
@@ -487,6 +623,7 @@ def main():
             "TFLOP/s": lay["matmul_TFLOPs"], "frac_of_fp8_peak": lay["matmul_frac_of_peak"],
             "layer_speedup_vs_rmsnorm_gamma_cast": lay["layer_speedup"],
             "layer_speedup_from_parts": lay["layer_speedup_from_parts"]},
+        "backward_kernels": bwd,
         "copy_d2d_GBps": round(copy_gbps, 1),
         "stream_reference_GBps": ref,
         "frac_of_stream_reference": round(gbps / ref["mixed"], 4),

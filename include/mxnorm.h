@@ -216,8 +216,8 @@ mx_status mx_cast_t_fwd(const void *x, const float *rho, int64_t R, int64_t C, i
  * the forward returned.  grad_x: [T, d] float32 or bf16 (out_dtype).
  * Arithmetic: dXb exact in float, u summed in double, c = rho^3 u / d in
  * double rounded to float, grad_x = RN(RN(rho dXb) - RN(c x)); the
- * grad_gamma partial sums are float over 32 rows, then summed in double in a
- * fixed order (deterministic).  grad_gamma: float [d] or NULL (not computed);
+ * grad_gamma partial sums are float over at most 32 rows, then summed in
+ * double in a fixed order (deterministic for a given T).  grad_gamma: float [d] or NULL (not computed);
  * it needs `workspace`, caller-owned device memory of at least
  * mxnorm_ste_bwd_workspace_bytes(T, d) bytes (16-byte aligned), overwritten.
  * d a multiple of 8 and <= MXNORM_MAX_D; 16-byte alignment of x, grad_z,

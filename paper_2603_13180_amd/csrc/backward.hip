@@ -18,6 +18,8 @@
 
 #include <stdint.h>
 
+#include <algorithm>
+
 #include "mxnorm.h"
 #include "norm_cast.h"
 #include "status.h"
@@ -32,6 +34,7 @@ using namespace mxk;
 
 constexpr int CT_ROWS = 128; // tile rows (4 waves x one 32-row block)
 constexpr int CT_COLS = 64;  // tile columns (one per lane)
+constexpr int CT_TILES = 16; // most tiles per workgroup (a span of up to 2048 rows)
 
 struct CastTArgs {
     const uint16_t *x;
@@ -40,121 +43,160 @@ struct CastTArgs {
     uint8_t *scales;
     int64_t R, C;
     int mode;
+    int tiles; // tiles per span, 1 .. CT_TILES
 };
 
-// Workgroup (tile_r, tile_c): rows [128 tile_r, +128) and columns
-// [64 tile_c, +64) of x.  The tile is staged in LDS as it is in x (128 bytes
-// per row); wave w then casts rows 32w .. 32w+31, lane c column c: it reads
-// its 32 values down the column (one row of the tile per read, the 64 lanes
-// on 128 consecutive bytes, so no bank conflicts), scales them by rho,
-// decides the E8M0 byte from their absmax and writes 32 codes (E4M3: 32 B;
-// E2M1: 16 B) into row c0 + c of the transposed output.
+// Workgroup (span, tile_c) casts columns [64 tile_c, +64) over a span of
+// `tiles` x 128 rows, 128 rows at a time (the host sizes the span so that
+// the grid still fills the chip).  Each 128 x 64 tile is staged in
+// LDS as it is in x (128 bytes per row; the next tile's loads are already in
+// flight in registers); wave w then casts rows 32w .. 32w+31 of it, lane c
+// column c: it reads its 32 values down the column (the 64 lanes of a read
+// on 128 consecutive bytes: no bank conflicts), scales them by rho, decides
+// the E8M0 byte from their absmax and writes 32 codes (E4M3: 32 B; E2M1:
+// 16 B) into row c0 + c of the transposed output.  The span's 64 scale bytes
+// per column are gathered in LDS and written at the end, 64 contiguous
+// bytes per output row, rather than one scattered byte per tile.
 template <bool FP4>
 __global__ void __launch_bounds__(256) cast_t_kernel(CastTArgs A)
 {
     __shared__ __attribute__((aligned(16))) uint16_t tile[CT_ROWS * CT_COLS];
     __shared__ float rs[CT_ROWS];
+    __shared__ __attribute__((aligned(16))) uint8_t sb[CT_COLS][CT_TILES * 4];
 
     const int tid = threadIdx.x;
-    const int64_t r0 = (int64_t)blockIdx.y * CT_ROWS;
+    const int64_t span0 = (int64_t)blockIdx.y * CT_ROWS * A.tiles;
     const int64_t c0 = (int64_t)blockIdx.x * CT_COLS;
+    const int ntiles = (int)min((int64_t)A.tiles, (A.R - span0 + CT_ROWS - 1) / CT_ROWS);
+    const int w = tid >> 6, c = tid & 63;
+    const int64_t orow = c0 + c;
+    const bool col_ok = orow < A.C;
 
-    // stage: thread t moves 16-byte chunk t % 8 of rows t / 8 + 32 k
-    {
-        const int ch = tid & 7;
-        const bool col_ok = c0 + 8 * ch < A.C; // C % 8 == 0: whole chunks
+    // staging: thread t moves 16-byte chunk t % 8 of tile rows t / 8 + 32 k
+    const int ch = tid & 7;
+    const bool chunk_ok = c0 + 8 * ch < A.C; // C % 8 == 0: whole chunks
+    auto fetch = [&](int64_t r0, uint4 v[4]) {
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
             const int r = (tid >> 3) + 32 * k;
-            uint4 v = make_uint4(0u, 0u, 0u, 0u);
-            if (col_ok && r0 + r < A.R)
-                v = load_stream(reinterpret_cast<const uint4 *>(A.x + (r0 + r) * A.C + c0) + ch);
-            *reinterpret_cast<uint4 *>(&tile[r * CT_COLS + 8 * ch]) = v;
+            v[k] = (chunk_ok && r0 + r < A.R)
+                       ? load_stream(reinterpret_cast<const uint4 *>(A.x + (r0 + r) * A.C + c0) + ch)
+                       : make_uint4(0u, 0u, 0u, 0u);
         }
+    };
+    uint4 nxt[4];
+    fetch(span0, nxt);
+
+    for (int t = 0; t < ntiles; ++t) {
+        const int64_t r0 = span0 + (int64_t)t * CT_ROWS;
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+            *reinterpret_cast<uint4 *>(&tile[((tid >> 3) + 32 * k) * CT_COLS + 8 * ch]) = nxt[k];
         if (tid < CT_ROWS)
             rs[tid] = (A.rho && r0 + tid < A.R) ? A.rho[r0 + tid] : 1.0f;
-    }
-    __syncthreads();
+        __syncthreads();
+        if (t + 1 < ntiles)
+            fetch(r0 + CT_ROWS, nxt);
 
-    const int w = tid >> 6, c = tid & 63;
-    const int64_t rb = r0 + 32 * w; // first row of this wave's block
-    if (rb >= A.R || c0 + c >= A.C)
-        return;
-
-    // pass 1: the block absmax of the scaled values (integer max of the
-    // magnitude bits: NaN propagates); pass 2 re-reads the column from LDS
-    // and converts 8 values at a time, which keeps few registers live
-    const uint16_t *col = tile + 32 * w * CT_COLS + c;
-    const float *rr = rs + 32 * w;
-    auto value = [&](int i) {
-        const float v = __uint_as_float((uint32_t)col[i * CT_COLS] << 16);
-        return A.rho ? v * rr[i] : v;
-    };
-    uint32_t m = 0;
+        const int64_t rb = r0 + 32 * w; // first row of this wave's block
+        if (rb < A.R && col_ok) {
+            // pass 1: the block absmax of the scaled values (integer max of
+            // the magnitude bits: NaN propagates); pass 2 re-reads the column
+            // from LDS and converts a few values at a time
+            const uint16_t *col = tile + 32 * w * CT_COLS + c;
+            const float *rr = rs + 32 * w;
+            auto value = [&](int i) {
+                const float v = __uint_as_float((uint32_t)col[i * CT_COLS] << 16);
+                return A.rho ? v * rr[i] : v;
+            };
+            uint32_t m = 0;
 #pragma unroll 8
-    for (int i = 0; i < 32; ++i)
-        m = max(m, __float_as_uint(value(i)) & 0x7FFFFFFFu);
-    const float a = __uint_as_float(m);
-    const int64_t orow = c0 + c;
+            for (int i = 0; i < 32; ++i)
+                m = max(m, __float_as_uint(value(i)) & 0x7FFFFFFFu);
+            const float a = __uint_as_float(m);
+            uint32_t byte;
+            if constexpr (!FP4) {
+                byte = e8m0_byte<false>(a, A.mode);
+                // FLOOR: |t| <= 448 * 2^e, saturate before the conversion
+                // (RCEIL never exceeds it)
+                const float lim = A.mode == MX_SCALE_FLOOR
+                                      ? __uint_as_float(((byte + 8u) << 23) | 0x600000u)
+                                      : __builtin_inff();
+                const float scale = __uint_as_float(byte << 23);
+                uint32_t q[8];
+#pragma unroll
+                for (int k = 0; k < 8; ++k) {
+                    float v[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        v[e] = __builtin_amdgcn_fmed3f(value(4 * k + e), -lim, lim);
+                    q[k] = e4m3x4_hw(v[0], v[1], v[2], v[3], scale);
+                    if (byte == 0xFFu) { // non-finite input: input signs, all-ones magnitude
+                        uint32_t r = 0x7F7F7F7Fu;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            r |= ((uint32_t)col[(4 * k + e) * CT_COLS] >> 15) << (8 * e + 7);
+                        q[k] = r;
+                    }
+                }
+                uint4 *dst = reinterpret_cast<uint4 *>(A.codes + orow * A.R + rb);
+                dst[0] = make_uint4(q[0], q[1], q[2], q[3]);
+                dst[1] = make_uint4(q[4], q[5], q[6], q[7]);
+            } else {
+                // the scaled fp4 conversion divides by the scale's power of
+                // two, rounds to nearest even and saturates at 6
+                byte = e8m0_byte<true>(a, A.mode);
+                const float scale = __uint_as_float(byte << 23);
+                uint32_t q[4];
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    uint32_t p = 0;
+                    p = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(p, value(8 * k), value(8 * k + 1), scale, 0);
+                    p = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(p, value(8 * k + 2), value(8 * k + 3), scale, 1);
+                    p = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(p, value(8 * k + 4), value(8 * k + 5), scale, 2);
+                    p = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(p, value(8 * k + 6), value(8 * k + 7), scale, 3);
+                    if (byte == 0xFFu) {
+                        p = 0x77777777u;
+#pragma unroll
+                        for (int e = 0; e < 8; ++e)
+                            p |= ((uint32_t)col[(8 * k + e) * CT_COLS] >> 15) << (4 * e + 3);
+                    }
+                    q[k] = p;
+                }
+                *reinterpret_cast<uint4 *>(A.codes + orow * (A.R / 2) + rb / 2) =
+                    make_uint4(q[0], q[1], q[2], q[3]);
+            }
+            sb[c][4 * t + w] = (uint8_t)byte;
+        }
+        __syncthreads(); // the tile is overwritten next
+    }
 
-    if constexpr (!FP4) {
-        const uint32_t byte = e8m0_byte<false>(a, A.mode);
-        // FLOOR: |t| <= 448 * 2^e, saturate before the conversion (RCEIL
-        // never exceeds it)
-        const float lim = A.mode == MX_SCALE_FLOOR
-                              ? __uint_as_float(((byte + 8u) << 23) | 0x600000u)
-                              : __builtin_inff();
-        const float scale = __uint_as_float(byte << 23);
-        uint32_t q[8];
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-            float t[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-                t[e] = __builtin_amdgcn_fmed3f(value(4 * k + e), -lim, lim);
-            q[k] = e4m3x4_hw(t[0], t[1], t[2], t[3], scale);
-            if (byte == 0xFFu) { // non-finite input: the input's signs, all-ones magnitude
-                uint32_t r = 0x7F7F7F7Fu;
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    r |= ((uint32_t)col[(4 * k + e) * CT_COLS] >> 15) << (8 * e + 7);
-                q[k] = r;
-            }
+    // the span's scale bytes: column c has 4 per tile (fewer where R ends
+    // inside the span), written by the 4 threads of its row as 16-byte pieces
+    // when whole and aligned, else byte by byte
+    const int64_t nblk = min((int64_t)ntiles * 4, (A.R - span0) / 32);
+    const int cc = tid >> 2, part = tid & 3;
+    const int64_t srow = c0 + cc;
+    if (srow < A.C) {
+        uint8_t *dst = A.scales + srow * (A.R / 32) + span0 / 32;
+        const int lo = 16 * part;
+        if (lo + 16 <= nblk && (((uintptr_t)(dst + lo)) & 15) == 0) {
+            *reinterpret_cast<uint4 *>(dst + lo) = *reinterpret_cast<const uint4 *>(&sb[cc][lo]);
+        } else {
+            for (int k = lo; k < lo + 16 && k < nblk; ++k)
+                dst[k] = sb[cc][k];
         }
-        uint4 *dst = reinterpret_cast<uint4 *>(A.codes + orow * A.R + rb);
-        dst[0] = make_uint4(q[0], q[1], q[2], q[3]);
-        dst[1] = make_uint4(q[4], q[5], q[6], q[7]);
-        A.scales[orow * (A.R / 32) + rb / 32] = (uint8_t)byte;
-    } else {
-        // the scaled fp4 conversion divides by the scale's power of two,
-        // rounds to nearest even and saturates at 6
-        const uint32_t byte = e8m0_byte<true>(a, A.mode);
-        const float scale = __uint_as_float(byte << 23);
-        uint32_t q[4];
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            uint32_t p = 0;
-            p = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(p, value(8 * k), value(8 * k + 1), scale, 0);
-            p = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(p, value(8 * k + 2), value(8 * k + 3), scale, 1);
-            p = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(p, value(8 * k + 4), value(8 * k + 5), scale, 2);
-            p = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(p, value(8 * k + 6), value(8 * k + 7), scale, 3);
-            if (byte == 0xFFu) {
-                p = 0x77777777u;
-#pragma unroll
-                for (int e = 0; e < 8; ++e)
-                    p |= ((uint32_t)col[(8 * k + e) * CT_COLS] >> 15) << (4 * e + 3);
-            }
-            q[k] = p;
-        }
-        *reinterpret_cast<uint4 *>(A.codes + orow * (A.R / 2) + rb / 2) =
-            make_uint4(q[0], q[1], q[2], q[3]);
-        A.scales[orow * (A.R / 32) + rb / 32] = (uint8_t)byte;
     }
 }
 
 // ------------------------------------------------------------ STE rows --
 
-constexpr int STE_RPW = 32; // rows per workgroup (one partial row of grad_gamma each)
+// rows per workgroup (each writes one partial row of grad_gamma): 4 .. 32,
+// as many as keep about 512 workgroups
+inline int ste_rpw(int64_t T)
+{
+    return (int)std::max<int64_t>(4, std::min<int64_t>(32, (T + 511) / 512));
+}
 
 struct SteArgs {
     const uint16_t *x, *gz, *gamma;
@@ -162,6 +204,7 @@ struct SteArgs {
     void *gx;
     float *part; // [workgroups, d] grad_gamma partials, or NULL
     int64_t T;
+    int rpw;     // rows per workgroup
     int d, nc; // columns, 8-column chunks
 };
 
@@ -174,7 +217,7 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f)
 }
 
 // The workgroup of NT threads is one team: thread l holds 8-column chunks
-// j NT + l, j < CPL, of each row, and rows [32 b, 32 b + 32) are done one
+// j NT + l, j < CPL, of each row, and rows [rpw b, rpw b + rpw) are done one
 // after the other.  Per row: dXb = RN(gz gamma) (exact: a product of two
 // bf16 values fits in float), u = sum dXb x accumulated in double (exact
 // products) and reduced over the team through LDS; c = RN(rho^3 u / d)
@@ -207,8 +250,8 @@ __global__ void __launch_bounds__(NT) ste_bwd_kernel(SteArgs A)
                 gg[j][e] = 0.0f;
     }
 
-    const int64_t row0 = (int64_t)blockIdx.x * STE_RPW;
-    const int64_t rows = min((int64_t)STE_RPW, A.T - row0);
+    const int64_t row0 = (int64_t)blockIdx.x * A.rpw;
+    const int64_t rows = min((int64_t)A.rpw, A.T - row0);
     for (int64_t k = 0; k < rows; ++k) {
         const int64_t row = row0 + k;
         const uint4 *xr = reinterpret_cast<const uint4 *>(A.x + row * A.d);
@@ -319,23 +362,37 @@ __global__ void __launch_bounds__(NT) ste_bwd_kernel(SteArgs A)
     }
 }
 
-// grad_gamma[j] = sum over the P partial rows, in order, in double
-__global__ void __launch_bounds__(256) ggamma_reduce_kernel(const float *part, int64_t P, int d,
-                                                            float *out)
+// grad_gamma[j] = sum of the P partial rows, in double, in a fixed order:
+// block b sums columns [64 b, 64 b + 64); thread (g, c) adds rows g, g + 16,
+// g + 32, ... of column c in order, then the 16 partial sums are added in
+// order of g.  Deterministic, and 16 x 64 loads in flight per block.
+constexpr int RG = 16;
+__global__ void __launch_bounds__(1024) ggamma_reduce_kernel(const float *part, int64_t P, int d,
+                                                             float *out)
 {
-    const int j = blockIdx.x * 256 + threadIdx.x;
-    if (j >= d)
-        return;
+    __shared__ double red[RG][64];
+    const int c = threadIdx.x & 63, g = threadIdx.x >> 6;
+    const int j = blockIdx.x * 64 + c;
     double s = 0.0;
-    for (int64_t p = 0; p < P; ++p)
-        s += (double)part[p * d + j];
-    out[j] = (float)s;
+    if (j < d)
+#pragma unroll 4
+        for (int64_t p = g; p < P; p += RG)
+            s += (double)part[p * d + j];
+    red[g][c] = s;
+    __syncthreads();
+    if (g == 0 && j < d) {
+        double t = 0.0;
+#pragma unroll
+        for (int i = 0; i < RG; ++i)
+            t += red[i][c];
+        out[j] = (float)t;
+    }
 }
 
 template <int NT, int CPL, int OUT, bool GAM>
 hipError_t launch_ste(const SteArgs &A, hipStream_t st)
 {
-    const unsigned blocks = (unsigned)((A.T + STE_RPW - 1) / STE_RPW);
+    const unsigned blocks = (unsigned)((A.T + A.rpw - 1) / A.rpw);
     if (A.part)
         hipLaunchKernelGGL((ste_bwd_kernel<NT, CPL, OUT, GAM, true>), dim3(blocks), dim3(NT), 0,
                            st, A);
@@ -369,7 +426,7 @@ namespace {
 
 bool aligned(const void *p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
 
-int64_t ste_workgroups(int64_t T) { return (T + mxb::STE_RPW - 1) / mxb::STE_RPW; }
+int64_t ste_workgroups(int64_t T) { return (T + mxb::ste_rpw(T) - 1) / mxb::ste_rpw(T); }
 
 } // namespace
 
@@ -407,8 +464,14 @@ mx_status mx_cast_t_fwd(const void *x, const float *rho, int64_t R, int64_t C, i
     A.R = R;
     A.C = C;
     A.mode = scale_mode;
-    const dim3 grid((unsigned)((C + mxb::CT_COLS - 1) / mxb::CT_COLS),
-                    (unsigned)((R + mxb::CT_ROWS - 1) / mxb::CT_ROWS));
+    // tiles per workgroup: as many as keep about 1024 workgroups (longer
+    // spans write longer runs of scale bytes), at most CT_TILES
+    const int64_t col_tiles = (C + mxb::CT_COLS - 1) / mxb::CT_COLS;
+    const int64_t row_tiles = (R + mxb::CT_ROWS - 1) / mxb::CT_ROWS;
+    A.tiles = (int)std::max<int64_t>(1, std::min<int64_t>(mxb::CT_TILES,
+                                                          col_tiles * row_tiles / 1024));
+    const int64_t span = (int64_t)mxb::CT_ROWS * A.tiles;
+    const dim3 grid((unsigned)col_tiles, (unsigned)((R + span - 1) / span));
     if (grid.y > 65535u)
         return mxk::fail(MX_EUNSUPPORTED, "R too large for one launch");
     hipStream_t st = static_cast<hipStream_t>(stream);
@@ -469,6 +532,7 @@ mx_status mxnorm_ste_bwd(const void *x, const void *grad_z, const void *gamma, c
     A.gx = grad_x;
     A.part = grad_gamma ? static_cast<float *>(workspace) : nullptr;
     A.T = T;
+    A.rpw = mxb::ste_rpw(T);
     A.d = (int)d;
     A.nc = (int)(d / 8);
     hipStream_t st = static_cast<hipStream_t>(stream);
@@ -480,8 +544,8 @@ mx_status mxnorm_ste_bwd(const void *x, const void *grad_z, const void *gamma, c
         e = gamma ? mxb::launch_ste_out<MX_OUT_BF16, true>(A, st)
                   : mxb::launch_ste_out<MX_OUT_BF16, false>(A, st);
     if (e == hipSuccess && grad_gamma) {
-        hipLaunchKernelGGL(mxb::ggamma_reduce_kernel, dim3((unsigned)((d + 255) / 256)),
-                           dim3(256), 0, st, static_cast<const float *>(workspace),
+        hipLaunchKernelGGL(mxb::ggamma_reduce_kernel, dim3((unsigned)((d + 63) / 64)),
+                           dim3(1024), 0, st, static_cast<const float *>(workspace),
                            ste_workgroups(T), (int)d, grad_gamma);
         e = hipGetLastError();
     }
