@@ -79,6 +79,11 @@ def _load():
         "mxo_mxcast_gain": (None, [P, P, I64, I64, I, I, I, P, P]),
         "mxo_mxcast_t": (ctypes.c_int, [P, P, I64, I64, I, I, I, P, P]),
         "mxo_ste_bwd": (None, [P, P, P, P, I64, I64, P, P]),
+        "mxo_postround_f": (ctypes.c_double, [ctypes.c_double, I]),
+        "mxo_postround_finv_exact": (ctypes.c_double, [ctypes.c_double, I]),
+        "mxo_postround_lut": (None, [I, P, P]),
+        "mxo_postround_finv_lut": (ctypes.c_double, [ctypes.c_double, P, P]),
+        "mxo_mxnorm_postround_mx": (None, [P, I64, I64, I, I, F, I, P, P, P, P]),
         "mxo_mx_matmul": (ctypes.c_int, [P, P, P, P, I64, I64, I64, I, I, P]),
     }
     for name, (res, args) in sig.items():
@@ -383,3 +388,47 @@ def ste_bwd(x, gz, gamma, rho):
     gg = np.empty(d, np.float64)
     _load().mxo_ste_bwd(_ptr(x), _ptr(gz), _ptr(g), _ptr(r), T, d, _ptr(gx), _ptr(gg))
     return gx, gg
+
+
+# ------------------------------------------------------- post-round MXNorm --
+
+POSTROUND_A = 64
+
+
+def postround_f(sigma, B):
+    """f_B(sigma) = E[max_i r(|X_i|)], X_i ~ N(0, sigma^2), i < B (the
+    post-round appendix, with the difference read the right way round)."""
+    return float(_load().mxo_postround_f(float(sigma), int(B)))
+
+
+def postround_finv_exact(x, B):
+    return float(_load().mxo_postround_finv_exact(float(x), int(B)))
+
+
+def postround_lut(B):
+    """(x_i, v_i), i = 0 .. A: x_i = RN32(2^(i/A)), v_i = RN32(f_B^-1(x_i))."""
+    xs = np.empty(POSTROUND_A + 1, np.float32)
+    vs = np.empty(POSTROUND_A + 1, np.float32)
+    _load().mxo_postround_lut(int(B), _ptr(xs), _ptr(vs))
+    return xs, vs
+
+
+def postround_finv_lut(X, B, lut=None):
+    xs, vs = postround_lut(B) if lut is None else lut
+    return float(_load().mxo_postround_finv_lut(float(X), _ptr(xs), _ptr(vs)))
+
+
+def mxnorm_postround_mx(x, B=32, elem="e4m3", eps=1e-6, mode="rceil"):
+    """Post-round MXNorm: rho~ from the power-of-two-rounded block absmaxes
+    through f^-1 (the post-round appendix), then Algorithm 2's cast.
+    Returns (codes, scales, rho32, sigma64)."""
+    x = _as_bf16_rows(x)
+    T, d = x.shape
+    cshape, sshape = _mx_shapes(T, d, B, elem)
+    codes = np.empty(cshape, np.uint8)
+    scales = np.empty(sshape, np.uint8)
+    r32 = np.empty(T, np.float32)
+    s64 = np.empty(T, np.float64)
+    _load().mxo_mxnorm_postround_mx(_ptr(x), T, d, B, ELEMS[elem], eps, SCALE_MODES[mode],
+                                    _ptr(codes), _ptr(scales), _ptr(r32), _ptr(s64))
+    return codes, scales, r32, s64

@@ -791,3 +791,145 @@ void mxo_ste_bwd(const uint16_t *x, const uint16_t *gz, const uint16_t *gamma, c
         }
     }
 }
+
+/* ------------------------------------------------------------------------ */
+/* Post-round MXNorm (the post-round appendix): the RMS estimated from the    */
+/* block absmaxes rounded down to powers of two, through the inverse of      */
+/* f(sigma) = E[max_i r(|X_i|)], X_i ~ N(0, sigma^2) iid, i < B.             */
+/*                                                                          */
+/* Readings (parity unpinned where the paper gives no value):               */
+/*  P1  the appendix's final difference is printed reversed (it would make  */
+/*      every probability negative) and one exponent reads N for the block  */
+/*      size: P(max r = 2^j) = F(2^(j+1)/sigma)^B - F(2^j/sigma)^B with     */
+/*      F(x) = P(|X| < x / sigma ... ) = erf(x / sqrt 2) for unit variance. */
+/*  P2  the series is summed for j = -64 .. 64 (the terms outside are below */
+/*      double precision for the sigmas the table needs).                   */
+/*  P3  A = 64 table intervals; points x_i = 2^(i/A) and values             */
+/*      v_i = f^-1(x_i), both rounded to float; f^-1 between them by linear */
+/*      interpolation in x; f^-1(2^k y) = 2^k f^-1(y) for y in [1, 2).      */
+/*  P4  r(0) = 0 (a block of zeros adds nothing); the row mean of r(m~)     */
+/*      over its K blocks is Xbar; sigma = f^-1(Xbar); rho~ =               */
+/*      (sigma^2 + eps)^(-1/2) as in R3 (a zero radicand gives 0); then the */
+/*      cast exactly as Algorithm 2 (R6).                                   */
+/* ------------------------------------------------------------------------ */
+
+#define MXO_PR_J 64
+#define MXO_PR_A 64
+
+/* r(x) = 2^floor(log2 x) for x > 0 (also subnormal x), 0 for x = 0,
+ * x itself for Inf/NaN */
+static double pow2_floor(double x)
+{
+    int e;
+    if (x == 0.0 || !isfinite(x))
+        return x;
+    frexp(x, &e); /* x = m 2^e, m in [0.5, 1) */
+    return ldexp(1.0, e - 1);
+}
+
+/* f_B(sigma), the series above in index order */
+double mxo_postround_f(double sigma, int B)
+{
+    double s = 0.0;
+    int j;
+    for (j = -MXO_PR_J; j <= MXO_PR_J; j++) {
+        const double hi = pow(erf(ldexp(1.0, j + 1) / sigma / sqrt(2.0)), (double)B);
+        const double lo = pow(erf(ldexp(1.0, j) / sigma / sqrt(2.0)), (double)B);
+        s += ldexp(1.0, j) * (hi - lo);
+    }
+    return s;
+}
+
+/* f_B^-1(x) by bisection (f is increasing): 200 halvings of a bracket */
+double mxo_postround_finv_exact(double x, int B)
+{
+    double lo = x / 16.0, hi = x * 16.0;
+    int i;
+    for (i = 0; i < 200; i++) {
+        const double mid = 0.5 * (lo + hi);
+        if (mid == lo || mid == hi)
+            break;
+        if (mxo_postround_f(mid, B) < x)
+            lo = mid;
+        else
+            hi = mid;
+    }
+    return 0.5 * (lo + hi);
+}
+
+/* the table of P3: xs[i], vs[i] for i = 0 .. A */
+void mxo_postround_lut(int B, float *xs, float *vs)
+{
+    int i;
+    for (i = 0; i <= MXO_PR_A; i++) {
+        const double x = exp2((double)i / MXO_PR_A);
+        xs[i] = (float)x;
+        vs[i] = (float)mxo_postround_finv_exact((double)xs[i], B);
+    }
+}
+
+/* f_B^-1 through the table (P3); X >= 0.  Non-finite X passes through. */
+double mxo_postround_finv_lut(double X, const float *xs, const float *vs)
+{
+    int e, i;
+    double y, t, v;
+    if (X == 0.0 || !isfinite(X))
+        return X;
+    y = 2.0 * frexp(X, &e); /* X = y 2^(e-1), y in [1, 2) */
+    i = 0;
+    while (i + 1 < MXO_PR_A && (double)xs[i + 1] <= y)
+        i++;
+    t = (y - (double)xs[i]) / ((double)xs[i + 1] - (double)xs[i]);
+    v = (double)vs[i] + t * ((double)vs[i + 1] - (double)vs[i]);
+    return ldexp(v, e - 1);
+}
+
+/* Post-round MXNorm with a general MX output (as mxo_mxnorm_mx, with the
+ * post-round estimate in place of Algorithm 2's generalised mean) */
+void mxo_mxnorm_postround_mx(const uint16_t *x, int64_t T, int64_t d, int B, int elem, float eps,
+                             int mode, uint8_t *codes, uint8_t *scales, float *rho32,
+                             double *sigma64)
+{
+    int64_t K = d / B, t, k;
+    float xs[MXO_PR_A + 1], vs[MXO_PR_A + 1];
+    float xf[64];
+    float m[4096];
+    uint8_t rowcodes[65536];
+    mxo_postround_lut(B, xs, vs);
+    for (t = 0; t < T; t++) {
+        const uint16_t *xr = x + t * d;
+        double S = 0.0, sigma, u, rho_d;
+        float rho_f;
+        for (k = 0; k < K; k++) {
+            int b;
+            for (b = 0; b < B; b++)
+                xf[b] = mxo_bf16_to_float(xr[k * B + b]);
+            m[k] = block_absmax(xf, B);
+            S += pow2_floor((double)m[k]); /* the rounded block scale factors */
+        }
+        sigma = mxo_postround_finv_lut(S / (double)K, xs, vs);
+        u = sigma * sigma + (double)eps;
+        rho_d = (u == 0.0) ? 0.0 : 1.0 / sqrt(u);
+        rho_f = (float)rho_d;
+        if (sigma64) sigma64[t] = sigma;
+        if (rho32) rho32[t] = rho_f;
+        for (k = 0; k < K; k++) {
+            float a = m[k] * rho_f;
+            int e, b;
+            uint8_t byte = e8m0_byte_for(a, mode, elem, &e);
+            scales[t * K + k] = byte;
+            for (b = 0; b < B; b++) {
+                uint16_t xb = xr[k * B + b];
+                uint8_t *c = rowcodes + k * B + b;
+                if (byte == 0xFF) {
+                    *c = elem_nan_code(sign_of_bf16(xb), elem);
+                } else {
+                    float tv = mxo_bf16_to_float(xb) * rho_f;
+                    float v = (float)ldexp((double)tv, -e);
+                    *c = elem_encode(v, elem);
+                }
+            }
+        }
+        store_row_codes(rowcodes, d, elem, codes + t * (elem == MXO_ELEM_E2M1 ? d / 2 : d));
+    }
+}
