@@ -497,6 +497,10 @@ def main():
     def rms(i):
         mxnorm.rmsnorm_mxfp8_fwd(xs[i], None, codes=codes[i], scales=scales[i], rho=rho[i])
 
+    def post(i):
+        mxnorm.mxnorm_postround_mx_fwd(xs[i], 32, "e4m3", codes=codes[i], scales=scales[i],
+                                       rho=rho[i])
+
     def rms_g(i):
         mxnorm.rmsnorm_mxfp8_fwd(xs[i], g, codes=codes[i], scales=scales[i], rho=rho[i])
 
@@ -522,6 +526,7 @@ def main():
     # every kernel, in interleaved rounds so that clock and thermal drift hit
     # all of them alike; the speedups use the per-kernel medians
     kernels = (("mxnorm_mxfp8", mxn, b8), ("rmsnorm_mxfp8", rms, b8),
+               ("mxnorm_postround_mxfp8", post, b8),
                ("rmsnorm_mxfp8_gamma", rms_g, b8 + 2 * d),
                ("mxnorm_nvfp4", nv_mxn, nvfp4_bytes(T, d)),
                ("rmsnorm_nvfp4", nv_rms, nvfp4_bytes(T, d)),

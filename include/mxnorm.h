@@ -137,6 +137,29 @@ mx_status mxnorm_mx_fwd(const void *x, int64_t T, int64_t d, int block, int elem
                         float coef, float eps, int scale_mode, uint8_t *codes, uint8_t *scales,
                         float *rho, void *stream);
 
+/*
+ * Post-round MXNorm (the post-round appendix; an ablation the paper reports
+ * unstable in training): the RMS is estimated from the block absmaxes
+ * rounded down to powers of two, r(m~) = 2^floor(log2 m~) (0 for an
+ * all-zero block), through the inverse of f(sigma) = E[max_i r(|X_i|)] for
+ * `block` independent N(0, sigma^2) values:  Xbar = (1/K) sum_k r(m~_k);
+ * sigma = f^-1(Xbar), read from a 65-point table on [1, 2] at x_i =
+ * 2^(i/64) by linear interpolation in x, scaled by the power of two that
+ * brings Xbar into [1, 2) (f(2 sigma) = 2 f(sigma));  rho~ = (sigma^2 +
+ * eps)^(-1/2) (a zero radicand gives 0).  Then the cast of mxnorm_mx_fwd
+ * (Algorithm 2).  The table is computed once per block size from the
+ * appendix's series in double (sum over j = -64..64) by bisection, values
+ * rounded to float; mxnorm_postround_table returns it.  Arguments as
+ * mxnorm_mx_fwd without p and coef.
+ */
+mx_status mxnorm_postround_mx_fwd(const void *x, int64_t T, int64_t d, int block, int elem,
+                                  float eps, int scale_mode, uint8_t *codes, uint8_t *scales,
+                                  float *rho, void *stream);
+
+/* The post-round table for `block` (16, 32, 64): x[i] = RN32(2^(i/64)),
+ * v[i] = RN32(f^-1(x[i])), i = 0..64; host arrays of 65 floats. */
+int mxnorm_postround_table(int block, float *x, float *v);
+
 /* RMSNorm (+ optional gain) then the general MX cast (Algorithm 1). */
 mx_status rmsnorm_mx_fwd(const void *x, const void *gamma, int64_t T, int64_t d, int block,
                          int elem, float eps, int scale_mode, uint8_t *codes, uint8_t *scales,

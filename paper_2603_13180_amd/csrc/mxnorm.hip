@@ -34,6 +34,9 @@
 #include "norm_cast.h"
 #include "status.h"
 
+#include <cmath>
+#include <mutex>
+
 namespace mxk {
 
 hipError_t launch_norm_cast_MX8_B16(const Args &A, int kind, int TL, int CPL, hipStream_t stream);
@@ -174,6 +177,59 @@ mx_status run(Args A, int fmt, int kind, void *stream)
     return MX_OK;
 }
 
+// ----------------------------------------------------- post-round table --
+//
+// Post-round MXNorm estimates the RMS as f^-1(Xbar), Xbar the mean of the
+// block absmaxes rounded down to powers of two and f(sigma) = E[max_i
+// r(|X_i|)] for B independent N(0, sigma^2) values (the post-round
+// appendix):  f(sigma) = sum_j 2^j (P(|X| < 2^(j+1))^B - P(|X| < 2^j)^B),
+// P(|X| < x) = erf(x / (sigma sqrt 2)).  Because f(2 sigma) = 2 f(sigma) the
+// inverse is tabulated on [1, 2] at x_i = 2^(i/64) (values rounded to
+// float) and scaled by powers of two in the kernel.
+
+double series_f(double sigma, int B)
+{
+    double acc = 0.0;
+    for (int j = -64; j <= 64; ++j) {
+        const double a = std::pow(std::erf(std::ldexp(1.0, j + 1) / sigma / std::sqrt(2.0)), B);
+        const double b = std::pow(std::erf(std::ldexp(1.0, j) / sigma / std::sqrt(2.0)), B);
+        acc += std::ldexp(1.0, j) * (a - b);
+    }
+    return acc;
+}
+
+// f is increasing: halve a bracket around x until it stops shrinking
+double series_f_inverse(double x, int B)
+{
+    double lo = x / 16.0, hi = x * 16.0;
+    for (int it = 0; it < 200; ++it) {
+        const double mid = 0.5 * (lo + hi);
+        if (mid == lo || mid == hi)
+            break;
+        (series_f(mid, B) < x ? lo : hi) = mid;
+    }
+    return 0.5 * (lo + hi);
+}
+
+struct PostTable {
+    float x[65], v[65];
+};
+
+// The table for block size B (16, 32 or 64), computed once per process.
+const PostTable &post_table(int B)
+{
+    static std::once_flag once[3];
+    static PostTable tab[3];
+    const int k = B == 16 ? 0 : B == 32 ? 1 : 2;
+    std::call_once(once[k], [&] {
+        for (int i = 0; i <= 64; ++i) {
+            tab[k].x[i] = (float)std::exp2((double)i / 64.0);
+            tab[k].v[i] = (float)series_f_inverse((double)tab[k].x[i], B);
+        }
+    });
+    return tab[k];
+}
+
 // The MX format for a block size and element format, or -1.
 int mx_format(int block, int elem)
 {
@@ -307,6 +363,44 @@ mx_status mxnorm_mx_fwd(const void *x, int64_t T, int64_t d, int block, int elem
     return run(make_args(x, nullptr, T, d, block, p, coef, eps, scale_mode, 1.0f, codes, scales,
                          rho),
                fmt, K_MXN, stream);
+}
+
+mx_status mxnorm_postround_mx_fwd(const void *x, int64_t T, int64_t d, int block, int elem,
+                                  float eps, int scale_mode, uint8_t *codes, uint8_t *scales,
+                                  float *rho, void *stream)
+{
+    clear_error();
+    const int fmt = mx_format(block, elem);
+    if (fmt < 0)
+        return fail(MX_EINVAL, "block must be 16, 32 or 64 and elem E4M3 or E2M1");
+    mx_status st = check_common(x, nullptr, T, d, block, eps, codes, scales, rho);
+    if (st != MX_OK)
+        return st;
+    if (scale_mode != MX_SCALE_RCEIL && scale_mode != MX_SCALE_FLOOR)
+        return fail(MX_EINVAL, "unknown scale_mode %d", scale_mode);
+    Args A = make_args(x, nullptr, T, d, block, 1, 1.0f, eps, scale_mode, 1.0f, codes, scales,
+                       rho);
+    const PostTable &tab = post_table(block);
+    for (int i = 0; i <= 64; ++i) {
+        A.pr_x[i] = tab.x[i];
+        A.pr_v[i] = tab.v[i];
+    }
+    return run(A, fmt, K_MXN_POST, stream);
+}
+
+int mxnorm_postround_table(int block, float *x, float *v)
+{
+    clear_error();
+    if (block != 16 && block != 32 && block != 64)
+        return fail(MX_EINVAL, "block must be 16, 32 or 64");
+    if (!x || !v)
+        return fail(MX_EINVAL, "x and v must be non-NULL");
+    const PostTable &tab = post_table(block);
+    for (int i = 0; i <= 64; ++i) {
+        x[i] = tab.x[i];
+        v[i] = tab.v[i];
+    }
+    return MX_OK;
 }
 
 mx_status rmsnorm_mx_fwd(const void *x, const void *gamma, int64_t T, int64_t d, int block,

@@ -32,6 +32,8 @@ struct Args {
     int mode;   // MX_SCALE_RCEIL or MX_SCALE_FLOOR
     float s_g;  // NVFP4 tensor decode scale
     int sw;     // bytes per scale store: 16, 4 or 1 (set from K and alignment)
+    // post-round MXNorm: the inverse of f on [1, 2] at x_i = 2^(i/64)
+    float pr_x[65], pr_v[65];
 };
 
 // ---------------------------------------------------------------- helpers --
@@ -203,6 +205,41 @@ __device__ __forceinline__ float rho_rms(double S, int d, float eps)
     return (u == 0.0) ? 0.0f : (float)(1.0 / sqrt(u));
 }
 
+// r(m~) = 2^floor(log2 m~) of a bf16 block absmax given as its 16-bit
+// magnitude pattern, as float bits: the exponent field alone for normal
+// values, the highest set significand bit for subnormals; 0 stays 0 and
+// Inf/NaN pass through.
+__device__ __forceinline__ uint32_t pow2_floor_bits(uint32_t m)
+{
+    const uint32_t u = m << 16;
+    if (u >= 0x7F800000u)
+        return u;
+    if (u & 0x7F800000u)
+        return u & 0x7F800000u;
+    return u ? (0x80000000u >> __builtin_clz(u)) : 0u;
+}
+
+// Post-round MXNorm's rho~ from Xbar, the mean of r(m~) over the row's
+// blocks (the post-round appendix): sigma = f^-1(Xbar) with Xbar = y 2^k,
+// y in [1, 2), f^-1(y) interpolated linearly between the table points that
+// bracket y, times 2^k; rho~ = (sigma^2 + eps)^(-1/2) in double, rounded to
+// float (a zero radicand gives 0).
+__device__ __forceinline__ float rho_postround(double X, const float *px, const float *pv, float eps)
+{
+    double sigma = X;
+    if (X != 0.0 && X <= DBL_MAX) {
+        int e;
+        const double y = 2.0 * frexp(X, &e);
+        int i = 0;
+        while (i + 1 < 64 && (double)px[i + 1] <= y)
+            ++i;
+        const double t = (y - (double)px[i]) / ((double)px[i + 1] - (double)px[i]);
+        sigma = ldexp((double)pv[i] + t * ((double)pv[i + 1] - (double)pv[i]), e - 1);
+    }
+    const double u = sigma * sigma + (double)eps;
+    return (u == 0.0) ? 0.0f : (float)(1.0 / sqrt(u));
+}
+
 // Sum of one double per lane over a team of TL lanes.  Butterfly inside the
 // wave (every lane ends with the same bits: each step adds the same two
 // values), then, for multi-wave teams, per-wave partials through LDS.
@@ -270,7 +307,7 @@ __device__ __forceinline__ void load_row(const Args &A, int64_t row, int l, int 
 // What a kernel computes before the cast: RMSNorm (Alg. 1), MXNorm (Alg. 2),
 // or nothing (the plain MX cast of x, or of x * gamma -- the gain-folded weight
 // cast MXCast(W gamma) of the MXNormLinear forward, Sec. 3.7).
-enum Kind : int { K_RMS = 0, K_MXN = 1, K_CAST = 2 };
+enum Kind : int { K_RMS = 0, K_MXN = 1, K_CAST = 2, K_MXN_POST = 3 };
 
 // F: output format.  KIND: see Kind.  GAM: apply gamma (RMSNorm and cast).  Workgroup b handles rows b*TEAMS .. b*TEAMS+TEAMS-1, one per team.
 // (A persistent variant that prefetches each team's next row during the
@@ -280,7 +317,8 @@ template <int TL, int CPL, int F, int KIND, bool GAM>
 __global__ void __launch_bounds__(Team<TL>::BLOCK)
 norm_cast_kernel(Args A)
 {
-    constexpr bool MXN = KIND == K_MXN;
+    constexpr bool POST = KIND == K_MXN_POST;
+    constexpr bool MXN = KIND == K_MXN || POST; // statistic from the block absmaxes
     constexpr bool CAST = KIND == K_CAST;
     constexpr int BLOCK = Team<TL>::BLOCK;
     constexpr int TEAMS = Team<TL>::TEAMS;
@@ -350,8 +388,12 @@ norm_cast_kernel(Args A)
                 mb[j] = m;
                 // every lane of the block adds its term: the sum is BL times
                 // the block sum, removed exactly (BL is a power of two) below
-                const double md = (double)__uint_as_float(m << 16);
-                s += (A.p == 1) ? md : md * md;
+                if constexpr (POST) {
+                    s += (double)__uint_as_float(pow2_floor_bits(m)); // r(m~)
+                } else {
+                    const double md = (double)__uint_as_float(m << 16);
+                    s += (A.p == 1) ? md : md * md;
+                }
             }
         } else if constexpr (!CAST) {
 #pragma unroll
@@ -380,7 +422,10 @@ norm_cast_kernel(Args A)
             s = team_sum<TL>(s, red, tid);
             if constexpr (MXN)
                 s *= 1.0 / BL;
-            rho = MXN ? rho_estimate(s, A.K, A.p, A.coef, A.eps) : rho_rms(s, A.d, A.eps);
+            if constexpr (POST)
+                rho = rho_postround(s / (double)A.K, A.pr_x, A.pr_v, A.eps);
+            else
+                rho = MXN ? rho_estimate(s, A.K, A.p, A.coef, A.eps) : rho_rms(s, A.d, A.eps);
             if (row_ok && l == 0 && A.rho)
                 A.rho[row] = rho;
         }
@@ -573,6 +618,10 @@ hipError_t launch_fmt(const Args &A, int kind, int TL, int CPL, hipStream_t stre
 {
     if (kind == K_MXN)
         return launch_kind<F, K_MXN, false>(A, TL, CPL, stream);
+    if constexpr (!Fmt<F>::NV) {
+        if (kind == K_MXN_POST)
+            return launch_kind<F, K_MXN_POST, false>(A, TL, CPL, stream);
+    }
     if (kind == K_CAST)
         return A.gamma ? launch_kind<F, K_CAST, true>(A, TL, CPL, stream)
                        : launch_kind<F, K_CAST, false>(A, TL, CPL, stream);

@@ -51,6 +51,8 @@ def load():
         "rmsnorm_nvfp4_fwd": (I, [P, P, I64, I64, F, F, P, P, P, P]),
         "mxnorm_mx_fwd": (I, [P, I64, I64, I, I, I, F, F, I, P, P, P, P]),
         "rmsnorm_mx_fwd": (I, [P, P, I64, I64, I, I, F, I, P, P, P, P]),
+        "mxnorm_postround_mx_fwd": (I, [P, I64, I64, I, I, F, I, P, P, P, P]),
+        "mxnorm_postround_table": (I, [I, P, P]),
         "mx_cast_fwd": (I, [P, P, I64, I64, I, I, I, P, P, P]),
         "mx_matmul_fwd": (I, [P, P, P, P, I64, I64, I64, I, I, P, I, P, P]),
         "mx_cast_t_fwd": (I, [P, P, I64, I64, I, I, I, P, P, P]),
@@ -202,6 +204,33 @@ def mxnorm_mx_fwd(x, block=32, elem="e4m3", p=2, coef=0.0, eps=1e-6, scale_mode=
                                 SCALE_MODES[scale_mode], _ptr(codes), _ptr(scales),
                                 _ptr(rho) if want_rho else None, _stream(x.device)))
     return codes, scales, (rho if want_rho else None)
+
+
+def mxnorm_postround_mx_fwd(x, block=32, elem="e4m3", eps=1e-6, scale_mode="rceil",
+                            codes=None, scales=None, rho=None, want_rho=True):
+    """Post-round MXNorm (the post-round appendix): rho~ from the block
+    absmaxes rounded down to powers of two, through the inverse of
+    f(sigma) = E[max r(|X|)], then the MX cast of Algorithm 2."""
+    T, d = _input(x)
+    cs, ss = _mx_out_shapes(T, d, block, elem)
+    codes = _out(codes, cs, torch.uint8, x.device)
+    scales = _out(scales, ss, torch.uint8, x.device)
+    if want_rho:
+        rho = _out(rho, (T,), torch.float32, x.device)
+    _check(load().mxnorm_postround_mx_fwd(_ptr(x), T, d, block, ELEMS[elem], eps,
+                                          SCALE_MODES[scale_mode], _ptr(codes), _ptr(scales),
+                                          _ptr(rho) if want_rho else None, _stream(x.device)))
+    return codes, scales, (rho if want_rho else None)
+
+
+def mxnorm_postround_table(block):
+    """The library's post-round table: (x, v) float32 arrays of 65 points."""
+    import numpy as np
+    xs = np.empty(65, np.float32)
+    vs = np.empty(65, np.float32)
+    _check(load().mxnorm_postround_table(block, xs.ctypes.data_as(ctypes.c_void_p),
+                                         vs.ctypes.data_as(ctypes.c_void_p)))
+    return xs, vs
 
 
 def rmsnorm_mx_fwd(x, gamma=None, block=32, elem="e4m3", eps=1e-6, scale_mode="rceil",

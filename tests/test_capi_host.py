@@ -237,3 +237,26 @@ def test_ste_rejects_bad_arguments(args, status):
     kw.update(args)
     assert lib.mxnorm_ste_bwd(kw["x"], kw["gz"], kw["gamma"], kw["rho"], kw["T"], kw["d"],
                               kw["out"], kw["gx"], kw["gg"], kw["ws"], kw["wsb"], None) == status
+
+
+@pytest.mark.parametrize("block", [16, 32, 64])
+def test_postround_table_equals_oracle_table(block):
+    # computed independently on both sides from the appendix's series; the
+    # float-rounded tables agree exactly, so the kernels and the oracle take
+    # rho~ from the same numbers
+    import oracle
+    xs, vs = mxnorm.mxnorm_postround_table(block)
+    ox, ov = oracle.postround_lut(block)
+    assert np.array_equal(xs, ox) and np.array_equal(vs, ov)
+
+
+def test_postround_validation():
+    lib = mxnorm.load()
+    assert lib.mxnorm_postround_table(8, OUT, OUT) == 1
+    # bad arguments only: every call below is rejected before any launch
+    assert lib.mxnorm_postround_mx_fwd(A16, 4, 64, 8, 0, 1e-6, 0, OUT, OUT, None, None) == 1
+    assert lib.mxnorm_postround_mx_fwd(A16, 4, 64, 32, 5, 1e-6, 0, OUT, OUT, None, None) == 1
+    assert lib.mxnorm_postround_mx_fwd(A16, 4, 48, 32, 0, 1e-6, 0, OUT, OUT, None, None) == 1
+    assert lib.mxnorm_postround_mx_fwd(A16, 4, 64, 32, 0, -1.0, 0, OUT, OUT, None, None) == 1
+    assert lib.mxnorm_postround_mx_fwd(A16, 4, 64, 32, 0, 1e-6, 7, OUT, OUT, None, None) == 1
+    assert lib.mxnorm_postround_mx_fwd(None, 0, 64, 32, 0, 1e-6, 0, None, None, None, None) == 0

@@ -504,3 +504,46 @@ def test_weight_cast_edge_rows(block, elem):
         gb = synth.f32_to_bf16_bits(np.linspace(-3, 3, d).astype(np.float32))
         check_cast(ab, gb, block, elem)
         check_cast(ab, None, block, elem, "floor")
+
+
+# ------------------------------------------------------- post-round MXNorm --
+
+def check_post(xb, block, elem, eps=1e-6, mode="rceil"):
+    x = dev_bf16(xb)
+    got = mxnorm.mxnorm_postround_mx_fwd(x, block=block, elem=elem, eps=eps, scale_mode=mode)
+    torch.cuda.synchronize()
+    wc, ws, w32, _ = oracle.mxnorm_postround_mx(xb, B=block, elem=elem, eps=eps, mode=mode)
+    codes, scales, rho = (t.cpu().numpy() for t in got)
+    ctx = "postround B=%d %s %s eps=%g shape=%s" % (block, elem, mode, eps, xb.shape)
+    same = (rho == w32) | (np.isnan(rho) & np.isnan(w32))
+    assert same.all(), "%s: rho differs in %d rows, first %s" % (ctx, (~same).sum(),
+                                                                  np.argwhere(~same)[0])
+    bad = np.argwhere(scales != ws)
+    assert bad.size == 0, "%s: %d scale bytes differ, first %s" % (ctx, len(bad), bad[0])
+    bad = np.argwhere(codes != wc)
+    assert bad.size == 0, "%s: %d codes differ, first %s" % (ctx, len(bad), bad[0])
+
+
+@pytest.mark.parametrize("block,elem", MX_FORMATS)
+@pytest.mark.parametrize("T,d", [(3, 64), (65, 192), (130, 1024), (33, 1280), (257, 4096),
+                                 (9, 10240), (4, 32768)])
+def test_postround_shapes(block, elem, T, d):
+    # rows with sigma spread over many octaves: every table segment and
+    # power-of-two scaling is exercised
+    rng = np.random.default_rng(T * d + block)
+    sig = np.exp2(rng.uniform(-20, 20, T)).astype(np.float32)
+    xb = synth.f32_to_bf16_bits((rng.standard_normal((T, d)) * sig[:, None]).astype(np.float32))
+    check_post(xb, block, elem)
+
+
+@pytest.mark.parametrize("block,elem", MX_FORMATS)
+def test_postround_modes_eps_and_edge_rows(block, elem):
+    xb = synth.gaussian(100, 2048, seed=block + 1, scale=0.3)
+    for mode in ("rceil", "floor"):
+        for eps in (0.0, 1e-6, 0.5):
+            check_post(xb, block, elem, eps=eps, mode=mode)
+    for d in (64, 1024):
+        ab = adversarial_rows(d, seed=block + d + 3)
+        for mode in ("rceil", "floor"):
+            for eps in (0.0, 1e-6):
+                check_post(ab, block, elem, eps=eps, mode=mode)
