@@ -13,7 +13,10 @@
 //      grad_x_j = rho dXb_j - (1/d) rho^3 u x_j,
 //    and grad_gamma_j = sum over rows of (rho x_j) grad_Z_j.
 //
-// Both are streaming kernels bound by HBM bandwidth.
+// Both are streaming kernels bound by HBM bandwidth.  Unlike the norm/cast
+// kernel they use ordinary stores: non-temporal ones measured slower here
+// (the column cast's 32-byte pieces of many rows rely on being merged in L2:
+// 3.3x slower with the hint; the STE 6% slower).
 #include <hip/hip_runtime.h>
 
 #include <stdint.h>

@@ -54,7 +54,9 @@ __global__ void __launch_bounds__(256) stream_kernel(const uint4 *x, int64_t T, 
         if (row_ok && j < cpl) {
             const int c = j * 64 + lane;
             const uint2 o = make_uint2((v[j].x >> 8) ^ v[j].y, (v[j].z >> 8) ^ v[j].w);
-            *reinterpret_cast<uint2 *>(out + rr * nc * 8 + (int64_t)c * 8) = o;
+            __builtin_nontemporal_store(((unsigned long long)o.y << 32) | o.x,
+                                        reinterpret_cast<unsigned long long *>(
+                                            out + rr * nc * 8 + (int64_t)c * 8));
             if ((lane & 3) == 0)
                 sb[c >> 2] = (uint8_t)v[j].x;
         }
@@ -63,9 +65,10 @@ __global__ void __launch_bounds__(256) stream_kernel(const uint4 *x, int64_t T, 
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     const int K = nc / 4;
+    typedef unsigned int u32x4v __attribute__((ext_vector_type(4)));
     if (row_ok && lane < K / 16)
-        *reinterpret_cast<uint4 *>(out_small + rr * K + 16 * lane) =
-            *reinterpret_cast<const uint4 *>(sb + 16 * lane);
+        __builtin_nontemporal_store(*reinterpret_cast<const u32x4v *>(sb + 16 * lane),
+                                    reinterpret_cast<u32x4v *>(out_small + rr * K + 16 * lane));
 }
 
 } // namespace
