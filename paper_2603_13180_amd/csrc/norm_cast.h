@@ -402,14 +402,12 @@ norm_cast_kernel(Args A)
 
         // ---- pass 1: the row statistic ----
         double s = 0.0;
-        uint32_t mb[MXN ? CPL : 1];
         if constexpr (MXN) {
 #pragma unroll
             for (int j = 0; j < CPL; ++j) {
                 if (j >= cpl)
                     break;
                 const uint32_t m = block_max<BL>(chunk_absmax_bits(v[j]));
-                mb[j] = m;
                 // every lane of the block adds its term: the sum is BL times
                 // the block sum, removed exactly (BL is a power of two) below
                 if constexpr (POST) {
@@ -478,7 +476,11 @@ norm_cast_kernel(Args A)
             // block maximum of |t|
             float a;
             if constexpr (MXN) {
-                a = __uint_as_float(mb[j] << 16) * rho; // = max |t| (RN is monotone)
+                // = max |t| (RN is monotone).  The block maximum is taken
+                // again from the raw row rather than kept from pass 1: the
+                // few max and DPP operations cost less than the registers,
+                // which keep the kernel at 8 waves per SIMD
+                a = __uint_as_float(block_max<BL>(chunk_absmax_bits(v[j])) << 16) * rho;
             } else {
                 // integer max of the magnitude patterns: NaN propagates
                 uint32_t m = 0;
