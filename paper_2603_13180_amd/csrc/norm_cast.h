@@ -314,17 +314,32 @@ struct Fmt {
     static constexpr int BL = B / 8;          // lanes (16-byte chunks) per block
 };
 
-// Chunks j*TL + l (j < cpl <= CPL) of `row` into v; zeros outside the tensor.
+// Chunks j*TL + l (j < CPL) of `row` into v; zeros outside the tensor.
+// Every load is issued, from an in-bounds address (chunk 0 of the row, or of
+// row 0, stands in for a chunk outside the tensor), and the zeros are
+// selected once the data is back.  A load under a per-lane condition instead
+// ends its branch with a wait for its own data, which leaves the wave one
+// 16-byte load in flight at a time (measured on MI355X: 5.8 against 6.5 TB/s
+// for the same traffic).  Chunks j >= cpl (uniformly absent) re-read a line
+// the row's first load brings into the cache.
 template <int TL, int CPL>
-__device__ __forceinline__ void load_row(const Args &A, int64_t row, int l, int cpl,
-                                         uint4 (&v)[CPL])
+__device__ __forceinline__ void load_row(const Args &A, int64_t row, int l, uint4 (&v)[CPL])
 {
     const bool row_ok = row < A.T;
     const uint4 *xr = reinterpret_cast<const uint4 *>(A.x + (row_ok ? row : 0) * A.d);
+    bool ok[CPL];
 #pragma unroll
     for (int j = 0; j < CPL; ++j) {
         const int c = j * TL + l;
-        v[j] = (j < cpl && row_ok && c < A.nc) ? load_stream(xr + c) : make_uint4(0u, 0u, 0u, 0u);
+        ok[j] = row_ok && c < A.nc;
+        v[j] = load_stream(xr + (ok[j] ? c : 0));
+    }
+#pragma unroll
+    for (int j = 0; j < CPL; ++j) {
+        v[j].x = ok[j] ? v[j].x : 0u;
+        v[j].y = ok[j] ? v[j].y : 0u;
+        v[j].z = ok[j] ? v[j].z : 0u;
+        v[j].w = ok[j] ? v[j].w : 0u;
     }
 }
 
@@ -382,7 +397,15 @@ norm_cast_kernel(Args A)
 #pragma unroll
         for (int j = 0; j < CPL; ++j) {
             const int c = j * TL + l;
-            g[j] = (c < A.nc) ? gr[c] : make_uint4(0u, 0u, 0u, 0u);
+            g[j] = gr[c < A.nc ? c : 0]; // unconditional, as in load_row
+        }
+#pragma unroll
+        for (int j = 0; j < CPL; ++j) {
+            const bool in = j * TL + l < A.nc;
+            g[j].x = in ? g[j].x : 0u;
+            g[j].y = in ? g[j].y : 0u;
+            g[j].z = in ? g[j].z : 0u;
+            g[j].w = in ? g[j].w : 0u;
         }
     }
 
@@ -392,7 +415,7 @@ norm_cast_kernel(Args A)
     uint4 v[CPL];
     {
         const int64_t row = (int64_t)blockIdx.x * TEAMS + team;
-        load_row<TL, CPL>(A, row, l, cpl, v);
+        load_row<TL, CPL>(A, row, l, v);
         const bool row_ok = row < A.T;
         const int64_t rr = row_ok ? row : 0;
         bool ok[CPL];

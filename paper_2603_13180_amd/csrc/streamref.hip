@@ -28,14 +28,26 @@ __global__ void __launch_bounds__(256) stream_kernel(const uint4 *x, int64_t T, 
     const bool row_ok = row < T;
     const int64_t rr = row_ok ? row : 0;
     const int cpl = nc / 64;
+    // loads issued unconditionally from in-bounds addresses, zeros selected
+    // afterwards (as the norm/cast kernel does): a load under a per-lane
+    // condition waits for its own data and serialises the wave's loads
     uint4 v[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
         if (MODE == MX_STREAM_WRITE)
             v[j] = make_uint4((uint32_t)rr, (uint32_t)j, (uint32_t)lane, 1u);
         else
-            v[j] = (row_ok && j < cpl) ? load_stream(x + rr * nc + j * 64 + lane)
-                                       : make_uint4(0u, 0u, 0u, 0u);
+            v[j] = load_stream(x + rr * nc + (j < cpl ? j * 64 : 0) + lane);
+    }
+    if (MODE != MX_STREAM_WRITE) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const bool ok = row_ok && j < cpl;
+            v[j].x = ok ? v[j].x : 0u;
+            v[j].y = ok ? v[j].y : 0u;
+            v[j].z = ok ? v[j].z : 0u;
+            v[j].w = ok ? v[j].w : 0u;
+        }
     }
     uint8_t *sb = sbuf + wave * 128;
     if (MODE == MX_STREAM_READ) {
