@@ -38,25 +38,6 @@ struct Args {
 
 // ---------------------------------------------------------------- helpers --
 
-// Streaming stores of the outputs: written once, never read back by the
-// kernel.  The non-temporal hint keeps them from displacing the input stream
-// in the caches (on MI355X: +8% for the MXFP8 kernels, +1..5% for MXFP4).
-typedef unsigned int u32x4v __attribute__((ext_vector_type(4)));
-__device__ __forceinline__ void store_nt8(uint8_t *p, uint32_t lo, uint32_t hi)
-{
-    __builtin_nontemporal_store(((unsigned long long)hi << 32) | lo,
-                                reinterpret_cast<unsigned long long *>(p));
-}
-__device__ __forceinline__ void store_nt4(uint8_t *p, uint32_t v)
-{
-    __builtin_nontemporal_store(v, reinterpret_cast<uint32_t *>(p));
-}
-__device__ __forceinline__ void store_nt16(uint8_t *p, const uint8_t *src)
-{
-    __builtin_nontemporal_store(*reinterpret_cast<const u32x4v *>(src),
-                                reinterpret_cast<u32x4v *>(p));
-}
-
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
@@ -211,7 +192,10 @@ __device__ __forceinline__ uint32_t sign_nibbles(uint4 v)
 // K blocks (Alg. 2; Sec. 3.4).  Double precision, rounded once to float.
 __device__ __forceinline__ float rho_estimate(double S, int K, int p, float coef, float eps)
 {
-    const double G = (p == 1) ? S / (double)K : sqrt(S / (double)K);
+    // S / K; for a power-of-two K the scaling is exact, so it equals the
+    // correctly rounded quotient without the division's latency
+    const double mean = (K & (K - 1)) == 0 ? ldexp(S, -__builtin_ctz((unsigned)K)) : S / (double)K;
+    const double G = (p == 1) ? mean : sqrt(mean);
     const double r = (double)coef * G;
     const double u = r * r + (double)eps;
     return (u == 0.0) ? 0.0f : (float)(1.0 / sqrt(u));
@@ -220,7 +204,8 @@ __device__ __forceinline__ float rho_estimate(double S, int K, int p, float coef
 // rho = ((1/d) sum x^2 + eps)^(-1/2) (Sec. 3.1 eq. (rms)).
 __device__ __forceinline__ float rho_rms(double S, int d, float eps)
 {
-    const double u = S / (double)d + (double)eps;
+    const double mean = (d & (d - 1)) == 0 ? ldexp(S, -__builtin_ctz((unsigned)d)) : S / (double)d;
+    const double u = mean + (double)eps;
     return (u == 0.0) ? 0.0f : (float)(1.0 / sqrt(u));
 }
 
@@ -264,16 +249,51 @@ __device__ __forceinline__ float rho_postround(double X, const float *px, const 
     return (u == 0.0) ? 0.0f : (float)(1.0 / sqrt(u));
 }
 
-// Sum of one double per lane over a team of TL lanes.  Butterfly inside the
-// wave (every lane ends with the same bits: each step adds the same two
-// values), then, for multi-wave teams, per-wave partials through LDS.
+// v from another lane by the DPP control CTRL, on both 32-bit halves; lanes
+// outside ROW_MASK's rows (or with no source lane) read 0.0.
+template <int CTRL, int ROW_MASK = 0xF>
+__device__ __forceinline__ double dpp_f64(double v)
+{
+    const unsigned long long b = __builtin_bit_cast(unsigned long long, v);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)b, CTRL, ROW_MASK, 0xF, false);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(b >> 32), CTRL, ROW_MASK, 0xF, false);
+    return __builtin_bit_cast(double, ((unsigned long long)hi << 32) | lo);
+}
+
+__device__ __forceinline__ double readlane_f64(double v, int lane)
+{
+    const unsigned long long b = __builtin_bit_cast(unsigned long long, v);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)b, lane);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(b >> 32), lane);
+    return __builtin_bit_cast(double, ((unsigned long long)hi << 32) | lo);
+}
+
+// Sum of one double per lane over a team of TL lanes; every lane of the team
+// gets the same bits.  Inside a 16-lane row: DPP quad permutes (lane i^1,
+// i^2) and the half-row and row mirrors, each step adding the same two values
+// on both lanes.  Across rows: row 15 broadcasts (rows 1 and 3 add row 0's and
+// row 2's sum, then rows 2 and 3 add lane 31's) and a read of the total's
+// lane.  Multi-wave teams join the per-wave sums through LDS.  No LDS round
+// trips inside a wave: the row statistic's latency is part of every row's
+// time.
 template <int TL>
 __device__ __forceinline__ double team_sum(double s, double *red, int tid)
 {
-    constexpr int W = TL < 64 ? TL : 64;
-#pragma unroll
-    for (int off = 1; off < W; off <<= 1)
-        s += __shfl_xor(s, off, W);
+    s += dpp_f64<0xB1>(s);  // quad_perm [1,0,3,2]
+    s += dpp_f64<0x4E>(s);  // quad_perm [2,3,0,1]
+    s += dpp_f64<0x141>(s); // row_half_mirror
+    s += dpp_f64<0x140>(s); // row_mirror
+    if constexpr (TL >= 32) {
+        s += dpp_f64<0x142, 0xA>(s); // row_bcast:15 into rows 1 and 3
+        if constexpr (TL == 32) {
+            // two teams per wave: rows 0-1 (total in lane 31), rows 2-3 (lane 63)
+            const double t0 = readlane_f64(s, 31), t1 = readlane_f64(s, 63);
+            s = (tid & 32) ? t1 : t0;
+        } else {
+            s += dpp_f64<0x143, 0xC>(s); // row_bcast:31 into rows 2 and 3
+            s = readlane_f64(s, 63);
+        }
+    }
     if constexpr (TL > 64) {
         constexpr int NW = TL / 64;
         const int wave = tid >> 6;
@@ -314,32 +334,39 @@ struct Fmt {
     static constexpr int BL = B / 8;          // lanes (16-byte chunks) per block
 };
 
-// Chunks j*TL + l (j < CPL) of `row` into v; zeros outside the tensor.
-// Every load is issued, from an in-bounds address (chunk 0 of the row, or of
-// row 0, stands in for a chunk outside the tensor), and the zeros are
-// selected once the data is back.  A load under a per-lane condition instead
-// ends its branch with a wait for its own data, which leaves the wave one
-// 16-byte load in flight at a time (measured on MI355X: 5.8 against 6.5 TB/s
-// for the same traffic).  Chunks j >= cpl (uniformly absent) re-read a line
-// the row's first load brings into the cache.
-template <int TL, int CPL>
-__device__ __forceinline__ void load_row(const Args &A, int64_t row, int l, uint4 (&v)[CPL])
+// Buffer resources.  A raw buffer access whose offset is at or past the
+// resource's byte count reads zeros (loads) or is dropped (stores) in the
+// hardware, so rows past T and chunks past the end of a row need no branch:
+// their offsets point past the end.  Each workgroup builds its resources
+// over its own rows, which keeps every offset far below 2^31.
+typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
+constexpr uint32_t kOutside = 0x80000000u; // an offset past every resource
+// Cache policy of the streaming accesses: each input byte is read once and
+// each output byte written once, never read back by the kernel, so both are
+// non-temporal; the hint keeps the outputs from displacing the input stream
+// in the caches (on MI355X: +8% for the MXFP8 kernels, +1..5% for MXFP4).
+constexpr int kBufNT = 2;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void *base, uint32_t bytes)
 {
-    const bool row_ok = row < A.T;
-    const uint4 *xr = reinterpret_cast<const uint4 *>(A.x + (row_ok ? row : 0) * A.d);
-    bool ok[CPL];
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, (int)bytes, 0x00020000);
+}
+
+// Chunks j*TL + l (j < CPL) of the team's row into v, zeros outside the
+// tensor.  All CPL loads issue back to back: a load under a per-lane branch
+// would end its branch with a wait for its own data and leave the wave one
+// 16-byte load in flight at a time (measured on MI355X: 5.8 against 6.5 TB/s
+// for the same traffic).
+template <int TL, int CPL>
+__device__ __forceinline__ void load_row(__amdgpu_buffer_rsrc_t xr, uint32_t row_off, int nc, int l,
+                                         uint4 (&v)[CPL])
+{
 #pragma unroll
     for (int j = 0; j < CPL; ++j) {
         const int c = j * TL + l;
-        ok[j] = row_ok && c < A.nc;
-        v[j] = load_stream(xr + (ok[j] ? c : 0));
-    }
-#pragma unroll
-    for (int j = 0; j < CPL; ++j) {
-        v[j].x = ok[j] ? v[j].x : 0u;
-        v[j].y = ok[j] ? v[j].y : 0u;
-        v[j].z = ok[j] ? v[j].z : 0u;
-        v[j].w = ok[j] ? v[j].w : 0u;
+        const uint32_t off = c < nc ? row_off + 16u * (uint32_t)c : kOutside;
+        const u32x4_t t = __builtin_amdgcn_raw_buffer_load_b128(xr, (int)off, 0, kBufNT);
+        v[j] = make_uint4(t.x, t.y, t.z, t.w);
     }
 }
 
@@ -348,12 +375,23 @@ __device__ __forceinline__ void load_row(const Args &A, int64_t row, int l, uint
 // cast MXCast(W gamma) of the MXNormLinear forward, Sec. 3.7).
 enum Kind : int { K_RMS = 0, K_MXN = 1, K_CAST = 2, K_MXN_POST = 3 };
 
+// Waves per SIMD the register allocation must allow.  A kernel that keeps
+// the row in registers and waits for it once per row hides that wait with
+// other waves: 8 per SIMD (64 VGPRs) fit the E8M0 kernels without spilling;
+// the gain, NVFP4 and multi-wave-team kernels need more registers and take
+// what they get.
+template <int TL, int F, bool GAM>
+constexpr int min_waves()
+{
+    return (GAM || Fmt<F>::NV || TL > 64) ? 1 : 8;
+}
+
 // F: output format.  KIND: see Kind.  GAM: apply gamma (RMSNorm and cast).  Workgroup b handles rows b*TEAMS .. b*TEAMS+TEAMS-1, one per team.
 // (A persistent variant that prefetches each team's next row during the
 // current one needs about twice the registers; at the resulting occupancy it
 // was slower for five of the six MXFP8/NVFP4 kernels on MI355X.)
 template <int TL, int CPL, int F, int KIND, bool GAM>
-__global__ void __launch_bounds__(Team<TL>::BLOCK)
+__global__ void __launch_bounds__(Team<TL>::BLOCK) __attribute__((amdgpu_waves_per_eu(min_waves<TL, F, GAM>())))
 norm_cast_kernel(Args A)
 {
     constexpr bool POST = KIND == K_MXN_POST;
@@ -393,19 +431,13 @@ norm_cast_kernel(Args A)
 
     uint4 g[GAM ? CPL : 1]; // gamma chunks: the same columns for every row
     if constexpr (GAM) {
-        const uint4 *gr = reinterpret_cast<const uint4 *>(A.gamma);
+        const __amdgpu_buffer_rsrc_t gr = buffer_rsrc(A.gamma, (uint32_t)A.d * 2u);
 #pragma unroll
         for (int j = 0; j < CPL; ++j) {
             const int c = j * TL + l;
-            g[j] = gr[c < A.nc ? c : 0]; // unconditional, as in load_row
-        }
-#pragma unroll
-        for (int j = 0; j < CPL; ++j) {
-            const bool in = j * TL + l < A.nc;
-            g[j].x = in ? g[j].x : 0u;
-            g[j].y = in ? g[j].y : 0u;
-            g[j].z = in ? g[j].z : 0u;
-            g[j].w = in ? g[j].w : 0u;
+            const uint32_t off = c < A.nc ? 16u * (uint32_t)c : kOutside;
+            const u32x4_t t = __builtin_amdgcn_raw_buffer_load_b128(gr, (int)off, 0, 0);
+            g[j] = make_uint4(t.x, t.y, t.z, t.w);
         }
     }
 
@@ -414,14 +446,18 @@ norm_cast_kernel(Args A)
     const int cpl = (A.nc + TL - 1) / TL;
     uint4 v[CPL];
     {
-        const int64_t row = (int64_t)blockIdx.x * TEAMS + team;
-        load_row<TL, CPL>(A, row, l, v);
+        const int64_t row0 = (int64_t)blockIdx.x * TEAMS; // the workgroup's first row
+        const int64_t row = row0 + team;
         const bool row_ok = row < A.T;
-        const int64_t rr = row_ok ? row : 0;
-        bool ok[CPL];
-#pragma unroll
-        for (int j = 0; j < CPL; ++j)
-            ok[j] = row_ok && (j * TL + l) < A.nc;
+        // rows of this workgroup inside the tensor, and the resources over them
+        const uint32_t rows = (uint32_t)min((int64_t)TEAMS, A.T - row0);
+        const uint32_t dcode = FP4 ? (uint32_t)A.d / 2u : (uint32_t)A.d; // code bytes per row
+        const __amdgpu_buffer_rsrc_t xr = buffer_rsrc(A.x + row0 * A.d, rows * (uint32_t)A.d * 2u);
+        const __amdgpu_buffer_rsrc_t cr = buffer_rsrc(A.codes + row0 * dcode, rows * dcode);
+        load_row<TL, CPL>(xr, (uint32_t)team * (uint32_t)A.d * 2u, A.nc, l, v);
+        // where this team's codes start in the store region; chunks past the
+        // row's end store nowhere (the hardware drops the access)
+        const uint32_t code_row = (uint32_t)team * dcode;
 
         // ---- pass 1: the row statistic ----
         double s = 0.0;
@@ -468,7 +504,9 @@ norm_cast_kernel(Args A)
             if constexpr (MXN)
                 s *= 1.0 / BL;
             if constexpr (POST)
-                rho = rho_postround(s / (double)A.K, A.pr_x, A.pr_v, A.eps);
+                rho = rho_postround((A.K & (A.K - 1)) == 0 ? ldexp(s, -__builtin_ctz((unsigned)A.K))
+                                                           : s / (double)A.K,
+                                    A.pr_x, A.pr_v, A.eps);
             else
                 rho = MXN ? rho_estimate(s, A.K, A.p, A.coef, A.eps) : rho_rms(s, A.d, A.eps);
             if (row_ok && l == 0 && A.rho)
@@ -531,11 +569,11 @@ norm_cast_kernel(Args A)
                         hi = nan_codes_e4m3(w[2], w[3]);
                     }
                 }
-                if (ok[j]) {
-                    store_nt8(A.codes + rr * A.d + (int64_t)c * 8, lo, hi);
-                    if ((l % BL) == 0)
-                        sb[c / BL] = (uint8_t)byte;
-                }
+                __builtin_amdgcn_raw_buffer_store_b64(
+                    (u32x2_t){lo, hi}, cr, (int)(c < A.nc ? code_row + 8u * (uint32_t)c : kOutside), 0,
+                    kBufNT);
+                if ((l % BL) == 0) // blocks past K are staged but never stored
+                    sb[c / BL] = (uint8_t)byte;
             } else if constexpr (!NV) {
                 // MXFP4: E2M1 codes of t / 2^e.  The scaled fp4 conversion
                 // divides by the scale operand's power of two, rounds to
@@ -553,11 +591,10 @@ norm_cast_kernel(Args A)
                     if (byte == 0xFFu)
                         packed = 0x77777777u | sign_nibbles(v[j]);
                 }
-                if (ok[j]) {
-                    store_nt4(A.codes + rr * (A.d / 2) + (int64_t)c * 4, packed);
-                    if ((l % BL) == 0)
-                        sb[c / BL] = (uint8_t)byte;
-                }
+                __builtin_amdgcn_raw_buffer_store_b32(
+                    packed, cr, (int)(c < A.nc ? code_row + 4u * (uint32_t)c : kOutside), 0, kBufNT);
+                if ((l % BL) == 0)
+                    sb[c / BL] = (uint8_t)byte;
             } else {
                 uint32_t S, packed = 0;
                 if (!(a <= FLT_MAX)) { // NaN or Inf block maximum
@@ -596,11 +633,10 @@ norm_cast_kernel(Args A)
                             packed |= e2m1_code(t[k] / den, t[k]) << (4 * k);
                     }
                 }
-                if (ok[j]) {
-                    store_nt4(A.codes + rr * (A.d / 2) + (int64_t)c * 4, packed);
-                    if ((l & 1) == 0)
-                        sb[c >> 1] = (uint8_t)S;
-                }
+                __builtin_amdgcn_raw_buffer_store_b32(
+                    packed, cr, (int)(c < A.nc ? code_row + 4u * (uint32_t)c : kOutside), 0, kBufNT);
+                if ((l & 1) == 0)
+                    sb[c >> 1] = (uint8_t)S;
             }
         }
 
@@ -613,12 +649,17 @@ norm_cast_kernel(Args A)
             __builtin_amdgcn_wave_barrier();
             __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
         }
-        if (row_ok) {
-            uint8_t *dst = A.scales + rr * A.K;
-            if (A.sw == 16) {
-                if (l < A.K / 16)
-                    store_nt16(dst + 16 * l, sb + 16 * l);
-            } else if (A.sw == 4) {
+        if (A.sw == 16) {
+            // K/16 lanes store 16 bytes each; rows past T store nowhere
+            const __amdgpu_buffer_rsrc_t sr = buffer_rsrc(A.scales + row0 * A.K, rows * (uint32_t)A.K);
+            const bool in = l < A.K / 16;
+            const u32x4_t val = *reinterpret_cast<const u32x4_t *>(sb + 16 * (in ? l : 0));
+            __builtin_amdgcn_raw_buffer_store_b128(
+                val, sr, (int)(in ? (uint32_t)team * (uint32_t)A.K + 16u * (uint32_t)l : kOutside), 0,
+                kBufNT);
+        } else if (row_ok) {
+            uint8_t *dst = A.scales + row * A.K;
+            if (A.sw == 4) {
                 for (int i = l; i < A.K / 4; i += TL)
                     *reinterpret_cast<uint32_t *>(dst + 4 * i) =
                         *reinterpret_cast<const uint32_t *>(sb + 4 * i);
