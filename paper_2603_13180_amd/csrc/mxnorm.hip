@@ -263,6 +263,10 @@ Args make_args(const void *x, const void *gamma, int64_t T, int64_t d, int block
     A.eps = eps;
     A.mode = mode;
     A.s_g = s_g;
+    // NVFP4: the scale quotient's divisor 6 s_g and its reciprocal, each one
+    // IEEE float rounding, once per launch rather than once per row
+    A.six_sg = 6.0f * s_g;
+    A.rcp_six_sg = A.six_sg > 0.0f ? 1.0f / A.six_sg : 0.0f;
     return A;
 }
 

@@ -31,6 +31,7 @@ struct Args {
     float eps;
     int mode;   // MX_SCALE_RCEIL or MX_SCALE_FLOOR
     float s_g;  // NVFP4 tensor decode scale
+    float six_sg, rcp_six_sg; // RN(6 s_g) and RN(1 / RN(6 s_g))
     int sw;     // bytes per scale store: 16, 4 or 1 (set from K and alignment)
     // post-round MXNorm: the inverse of f on [1, 2] at x_i = 2^(i/64)
     float pr_x[65], pr_v[65];
@@ -165,6 +166,20 @@ __device__ __forceinline__ float div_by_recip(float t, float den, float r)
     const float q0 = t * r;
     const float rem = __builtin_fmaf(-q0, den, t);
     return __builtin_fmaf(rem, r, q0);
+}
+
+// -(t / den) from r = 1/den as div_by_recip computes it, with the
+// correction applied as -rem * r + (-q0): for a nonzero quotient the single
+// rounding gives exactly the negated value, and a zero or underflowing
+// quotient comes out with the sign opposite to t's (q0 and rem carry the
+// sign of t), where rem * r + q0 would round an exact zero to +0.  Encoding
+// the negated quotients and flipping every code's sign bit afterwards keeps
+// the sign of t on zeros at one operation per eight codes.
+__device__ __forceinline__ float neg_div_by_recip(float t, float den, float r)
+{
+    const float q0 = t * r;
+    const float rem = __builtin_fmaf(-q0, den, t);
+    return __builtin_fmaf(-rem, r, -q0);
 }
 
 // Codes of a NaN block: each element's bf16 sign bit with an all-ones
@@ -418,8 +433,8 @@ norm_cast_kernel(Args A)
             const float den = e4m3_value(threadIdx.x) * A.s_g;
             den_tab[threadIdx.x] = make_float2(den, den >= 0x1p-90f ? 1.0f / den : 0.0f);
         }
-        six_sg = 6.0f * A.s_g;
-        rcp_six_sg = 1.0f / six_sg;
+        six_sg = A.six_sg;
+        rcp_six_sg = A.rcp_six_sg;
         six_sg_ok = six_sg >= 0x1p-90f;
         __syncthreads();
     }
@@ -613,16 +628,19 @@ norm_cast_kernel(Args A)
                     const float den = dr.x, r = dr.y;
                     if (r > 0.0f && a * r <= 0x1p100f) {
                         // common case: every quotient is finite and the
-                        // Markstein correction is exact; the sign is taken
-                        // from t so zero and underflowing quotients keep it
+                        // Markstein correction is exact.  The negated
+                        // quotients are encoded and the sign bits flipped
+                        // back, so zero and underflowing quotients keep the
+                        // sign of t
                         float vq[8];
 #pragma unroll
                         for (int k = 0; k < 8; ++k)
-                            vq[k] = __builtin_copysignf(div_by_recip(t[k], den, r), t[k]);
+                            vq[k] = neg_div_by_recip(t[k], den, r);
                         packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, vq[0], vq[1], 1.0f, 0);
                         packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, vq[2], vq[3], 1.0f, 1);
                         packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, vq[4], vq[5], 1.0f, 2);
                         packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, vq[6], vq[7], 1.0f, 3);
+                        packed ^= 0x88888888u;
                     } else if (den == 0.0f) {
 #pragma unroll
                         for (int k = 0; k < 8; ++k)
