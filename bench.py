@@ -38,8 +38,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=300,
-                    help="untimed launches first: the device takes about 200 back-to-back
-                         launches (~13 ms) to settle to its sustained rate")
+                    help="untimed launches first: the device takes about 200 back-to-back "
+                         "launches (~13 ms) to settle to its sustained rate")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--sweep", metavar="OUT_JSON",
                     help="instead of the headline line, run the paper's kernel sweep "
