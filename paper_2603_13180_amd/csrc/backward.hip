@@ -97,7 +97,7 @@ __global__ void __launch_bounds__(256) cast_t_kernel(CastTArgs A)
             *reinterpret_cast<uint4 *>(&tile[((tid >> 3) + 32 * k) * CT_COLS + 8 * ch]) = nxt[k];
         if (tid < CT_ROWS)
             rs[tid] = (A.rho && r0 + tid < A.R) ? A.rho[r0 + tid] : 1.0f;
-        __syncthreads();
+        lds_barrier();
         if (t + 1 < ntiles)
             fetch(r0 + CT_ROWS, nxt);
 
@@ -171,7 +171,7 @@ __global__ void __launch_bounds__(256) cast_t_kernel(CastTArgs A)
             }
             sb[c][4 * t + w] = (uint8_t)byte;
         }
-        __syncthreads(); // the tile is overwritten next
+        lds_barrier(); // the tile is overwritten next
     }
 
     // the span's scale bytes: column c has 4 per tile (fewer where R ends
@@ -220,28 +220,50 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f)
 }
 
 // The workgroup of NT threads is one team: thread l holds 8-column chunks
-// j NT + l, j < CPL, of each row, and rows [rpw b, rpw b + rpw) are done one
-// after the other.  Per row: dXb = RN(gz gamma) (exact: a product of two
+// j NT + l, j < CPL, of each row, and the workgroup's rows are done one
+// after the other, each row's x and grad_Z loads issued while the rows before
+// it are processed.  Per row: dXb = RN(gz gamma) (exact: a product of two
 // bf16 values fits in float), u = sum dXb x accumulated in double (exact
-// products) and reduced over the team through LDS; c = RN(rho^3 u / d)
-// computed in double; grad_x = RN(RN(rho dXb) - RN(c x)).  Each thread keeps
-// sum over its rows of RN(rho x) gz for its columns (float) and stores it as
-// this workgroup's partial row of grad_gamma.
+// products), reduced in the wave by DPP and over the team through LDS; c =
+// RN(rho^3 u / d) computed in double; grad_x = RN(RN(rho dXb) - RN(c x)).
+// Each thread keeps sum over its rows of RN(rho x) gz for its columns (float)
+// and stores it as this workgroup's partial row of grad_gamma.  Loads and
+// grad_x stores go through buffer resources, so chunks past the row's end
+// and rows past T read zeros and store nowhere
+// without a per-lane branch (which would serialise the loads).  Loads and
+// stores use one resource per row.
 template <int NT, int CPL, int OUT, bool GAM, bool GG>
-__global__ void __launch_bounds__(NT) ste_bwd_kernel(SteArgs A)
+__global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(NT * CPL <= 512 ? 4 : 1)))
+ste_bwd_kernel(SteArgs A)
 {
     constexpr int NW = NT / 64;
+    constexpr uint32_t OB = OUT == MX_OUT_F32 ? 4u : 2u; // grad_x bytes per element
     __shared__ double red[2][NW];
     const int tid = threadIdx.x;
     const int cpl = (A.nc + NT - 1) / NT; // chunks this row really has (uniform)
 
+    // workgroup b takes rows b, b + G, b + 2G, ... (G workgroups, all
+    // resident at once): the rows in flight across the chip at any moment
+    // form one contiguous band of the tensors rather than G separate streams
+    const int64_t G = gridDim.x;
+    const int rows = (int)((A.T - (int64_t)blockIdx.x + G - 1) / G);
+    const uint32_t rowb = (uint32_t)A.d * 2u; // bytes of a bf16 row
+    auto row_of = [&](int k) { return (int64_t)blockIdx.x + (int64_t)k * G; };
+    // byte offset of chunk j inside a bf16 row, or past every resource
+    uint32_t coff[CPL];
+#pragma unroll
+    for (int j = 0; j < CPL; ++j) {
+        const int ch = j * NT + tid;
+        coff[j] = ch < A.nc ? 16u * (uint32_t)ch : kOutside;
+    }
+
     uint4 g[GAM ? CPL : 1];
     if constexpr (GAM) {
+        const __amdgpu_buffer_rsrc_t gr = buffer_rsrc(A.gamma, rowb);
 #pragma unroll
         for (int j = 0; j < CPL; ++j) {
-            const int ch = j * NT + tid;
-            g[j] = (j < cpl && ch < A.nc) ? reinterpret_cast<const uint4 *>(A.gamma)[ch]
-                                          : make_uint4(0u, 0u, 0u, 0u);
+            const u32x4_t t = __builtin_amdgcn_raw_buffer_load_b128(gr, (int)coff[j], 0, 0);
+            g[j] = make_uint4(t.x, t.y, t.z, t.w);
         }
     }
     float gg[GG ? CPL : 1][8];
@@ -253,21 +275,29 @@ __global__ void __launch_bounds__(NT) ste_bwd_kernel(SteArgs A)
                 gg[j][e] = 0.0f;
     }
 
-    const int64_t row0 = (int64_t)blockIdx.x * A.rpw;
-    const int64_t rows = min((int64_t)A.rpw, A.T - row0);
-    for (int64_t k = 0; k < rows; ++k) {
-        const int64_t row = row0 + k;
-        const uint4 *xr = reinterpret_cast<const uint4 *>(A.x + row * A.d);
-        const uint4 *zr = reinterpret_cast<const uint4 *>(A.gz + row * A.d);
-        uint4 xv[CPL], zv[CPL];
+    // row k's x and grad_Z chunks and its rho (k >= rows: an empty resource,
+    // which reads zeros and moves no data).  rho travels with the row: a load
+    // issued later than the rows in flight would make its wait one for all
+    // of them (the vector memory counter completes in order)
+    auto load = [&](int k, uint4 (&xv)[CPL], uint4 (&zv)[CPL], float &rv) {
+        const int64_t row = k < rows ? row_of(k) : 0;
+        rv = k < rows ? A.rho[row] : 0.0f;
+        const uint32_t n = k < rows ? rowb : 0u;
+        const __amdgpu_buffer_rsrc_t xr = buffer_rsrc(A.x + row * A.d, n);
+        const __amdgpu_buffer_rsrc_t zr = buffer_rsrc(A.gz + row * A.d, n);
 #pragma unroll
         for (int j = 0; j < CPL; ++j) {
-            const int ch = j * NT + tid;
-            const bool ok = j < cpl && ch < A.nc;
-            xv[j] = ok ? load_stream(xr + ch) : make_uint4(0u, 0u, 0u, 0u);
-            zv[j] = ok ? load_stream(zr + ch) : make_uint4(0u, 0u, 0u, 0u);
+            const u32x4_t a = __builtin_amdgcn_raw_buffer_load_b128(xr, (int)coff[j], 0, kBufNT);
+            const u32x4_t b = __builtin_amdgcn_raw_buffer_load_b128(zr, (int)coff[j], 0, kBufNT);
+            xv[j] = make_uint4(a.x, a.y, a.z, a.w);
+            zv[j] = make_uint4(b.x, b.y, b.z, b.w);
         }
-        const float rho = A.rho[row];
+    };
+
+    auto process = [&](int k, const uint4 (&xv)[CPL], const uint4 (&zv)[CPL], const float rho) {
+        const int64_t row = row_of(k);
+        const __amdgpu_buffer_rsrc_t outr =
+            buffer_rsrc(static_cast<uint8_t *>(A.gx) + row * A.d * OB, (uint32_t)A.d * OB);
 
         // u = sum dXb x over the row
         double s = 0.0;
@@ -292,17 +322,15 @@ __global__ void __launch_bounds__(NT) ste_bwd_kernel(SteArgs A)
                 s = __builtin_fma((double)d1, (double)bf16_hi(xw[i]), s);
             }
         }
-#pragma unroll
-        for (int off = 1; off < 64; off <<= 1)
-            s += __shfl_xor(s, off, 64);
-        double *rb = red[k & 1]; // two buffers: one barrier per row suffices
+        s = team_sum<64>(s, nullptr, tid); // the wave's sum, in every lane
+        double *red_k = red[k & 1];        // two buffers: one barrier per row suffices
         if ((tid & 63) == 0)
-            rb[tid >> 6] = s;
-        __syncthreads();
+            red_k[tid >> 6] = s;
+        lds_barrier();
         double u = 0.0;
 #pragma unroll
         for (int i = 0; i < NW; ++i)
-            u += rb[i];
+            u += red_k[i];
         const double rd = (double)rho;
         const float cf = (float)(rd * rd * rd * u / (double)A.d);
 
@@ -310,7 +338,6 @@ __global__ void __launch_bounds__(NT) ste_bwd_kernel(SteArgs A)
         for (int j = 0; j < CPL; ++j) {
             if (j >= cpl)
                 break;
-            const int ch = j * NT + tid;
             const uint32_t xw[4] = {xv[j].x, xv[j].y, xv[j].z, xv[j].w};
             const uint32_t zw[4] = {zv[j].x, zv[j].y, zv[j].z, zv[j].w};
             uint32_t gw[4] = {0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u};
@@ -333,21 +360,49 @@ __global__ void __launch_bounds__(NT) ste_bwd_kernel(SteArgs A)
                     gg[j][2 * i + 1] += (rho * x1) * z1;
                 }
             }
-            if (ch < A.nc) {
-                if constexpr (OUT == MX_OUT_F32) {
-                    float4 *dst = reinterpret_cast<float4 *>(static_cast<float *>(A.gx) + row * A.d) +
-                                  2 * ch;
-                    dst[0] = make_float4(o[0], o[1], o[2], o[3]);
-                    dst[1] = make_float4(o[4], o[5], o[6], o[7]);
-                } else {
-                    uint32_t p[4];
+            // grad_x of chunk j: OB * 8 bytes at OB/2 times the bf16 offset
+            const uint32_t off = coff[j] == kOutside ? kOutside : coff[j] * (OB / 2u);
+            if constexpr (OUT == MX_OUT_F32) {
+                __builtin_amdgcn_raw_buffer_store_b128(
+                    (u32x4_t){__float_as_uint(o[0]), __float_as_uint(o[1]), __float_as_uint(o[2]),
+                              __float_as_uint(o[3])},
+                    outr, (int)off, 0, 0);
+                __builtin_amdgcn_raw_buffer_store_b128(
+                    (u32x4_t){__float_as_uint(o[4]), __float_as_uint(o[5]), __float_as_uint(o[6]),
+                              __float_as_uint(o[7])},
+                    outr, (int)(off == kOutside ? kOutside : off + 16u), 0, 0);
+            } else {
+                uint32_t p[4];
 #pragma unroll
-                    for (int i = 0; i < 4; ++i)
-                        p[i] = f32_to_bf16(o[2 * i]) | ((uint32_t)f32_to_bf16(o[2 * i + 1]) << 16);
-                    reinterpret_cast<uint4 *>(static_cast<uint16_t *>(A.gx) + row * A.d)[ch] =
-                        make_uint4(p[0], p[1], p[2], p[3]);
-                }
+                for (int i = 0; i < 4; ++i)
+                    p[i] = f32_to_bf16(o[2 * i]) | ((uint32_t)f32_to_bf16(o[2 * i + 1]) << 16);
+                __builtin_amdgcn_raw_buffer_store_b128((u32x4_t){p[0], p[1], p[2], p[3]}, outr, (int)off,
+                                                       0, 0);
             }
+        }
+    };
+
+    // two register sets: row k+1's loads are in flight while row k is
+    // processed; the widest teams (a 1024-thread workgroup has 128 registers
+    // per lane) hold one
+    if constexpr (NT * CPL <= 2048) {
+        uint4 xa[CPL], za[CPL], xb[CPL], zb[CPL];
+        float ra, rb;
+        load(0, xa, za, ra);
+        for (int k = 0; k < rows; k += 2) {
+            load(k + 1, xb, zb, rb);
+            process(k, xa, za, ra);
+            if (k + 1 >= rows)
+                break;
+            load(k + 2, xa, za, ra);
+            process(k + 1, xb, zb, rb);
+        }
+    } else {
+        uint4 xa[CPL], za[CPL];
+        float ra;
+        for (int k = 0; k < rows; ++k) {
+            load(k, xa, za, ra);
+            process(k, xa, za, ra);
         }
     }
 
@@ -365,31 +420,50 @@ __global__ void __launch_bounds__(NT) ste_bwd_kernel(SteArgs A)
     }
 }
 
-// grad_gamma[j] = sum of the P partial rows, in double, in a fixed order:
-// block b sums columns [64 b, 64 b + 64); thread (g, c) adds rows g, g + 16,
-// g + 32, ... of column c in order, then the 16 partial sums are added in
-// order of g.  Deterministic, and 16 x 64 loads in flight per block.
-constexpr int RG = 16;
-__global__ void __launch_bounds__(1024) ggamma_reduce_kernel(const float *part, int64_t P, int d,
-                                                             float *out)
+// grad_gamma[j] = sum of the P partial rows, in double, in a fixed order, in
+// two launches so that the first one spreads over the whole chip:
+//  * slice pass: block (b, s) sums columns [64 b, 64 b + 64) over partial
+//    rows [s Ps, (s + 1) Ps) (Ps = ceil(P / GG_SLICES)); thread (g, c) adds
+//    rows s Ps + g, + 4, + 8, ... of column c in order, the 4 sums are added
+//    in order of g and stored as the double slice[s][j];
+//  * final pass: grad_gamma[j] = RN(sum over s of slice[s][j], in order).
+// Deterministic; each wave reads 256 contiguous bytes per partial row.
+constexpr int GG_SLICES = 16;
+constexpr int GG_GROUPS = 4;
+__global__ void __launch_bounds__(256) ggamma_slice_kernel(const float *part, int64_t P, int d,
+                                                           double *slice)
 {
-    __shared__ double red[RG][64];
+    __shared__ double red[GG_GROUPS][64];
     const int c = threadIdx.x & 63, g = threadIdx.x >> 6;
     const int j = blockIdx.x * 64 + c;
+    const int64_t Ps = (P + GG_SLICES - 1) / GG_SLICES;
+    const int64_t p0 = (int64_t)blockIdx.y * Ps, p1 = min(P, p0 + Ps);
     double s = 0.0;
     if (j < d)
 #pragma unroll 4
-        for (int64_t p = g; p < P; p += RG)
+        for (int64_t p = p0 + g; p < p1; p += GG_GROUPS)
             s += (double)part[p * d + j];
     red[g][c] = s;
-    __syncthreads();
+    lds_barrier();
     if (g == 0 && j < d) {
         double t = 0.0;
 #pragma unroll
-        for (int i = 0; i < RG; ++i)
+        for (int i = 0; i < GG_GROUPS; ++i)
             t += red[i][c];
-        out[j] = (float)t;
+        slice[(int64_t)blockIdx.y * d + j] = t;
     }
+}
+
+__global__ void __launch_bounds__(256) ggamma_final_kernel(const double *slice, int d, float *out)
+{
+    const int j = blockIdx.x * 256 + threadIdx.x;
+    if (j >= d)
+        return;
+    double t = 0.0;
+#pragma unroll
+    for (int s = 0; s < GG_SLICES; ++s)
+        t += slice[(int64_t)s * d + j];
+    out[j] = (float)t;
 }
 
 template <int NT, int CPL, int OUT, bool GAM>
@@ -492,7 +566,9 @@ size_t mxnorm_ste_bwd_workspace_bytes(int64_t T, int64_t d)
 {
     if (T <= 0 || d <= 0)
         return 0;
-    return (size_t)ste_workgroups(T) * (size_t)d * sizeof(float);
+    // the workgroups' partial rows (float), then the reduction's slices (double)
+    return (size_t)ste_workgroups(T) * (size_t)d * sizeof(float) +
+           (size_t)mxb::GG_SLICES * (size_t)d * sizeof(double);
 }
 
 mx_status mxnorm_ste_bwd(const void *x, const void *grad_z, const void *gamma, const float *rho,
@@ -547,10 +623,19 @@ mx_status mxnorm_ste_bwd(const void *x, const void *grad_z, const void *gamma, c
         e = gamma ? mxb::launch_ste_out<MX_OUT_BF16, true>(A, st)
                   : mxb::launch_ste_out<MX_OUT_BF16, false>(A, st);
     if (e == hipSuccess && grad_gamma) {
-        hipLaunchKernelGGL(mxb::ggamma_reduce_kernel, dim3((unsigned)((d + 63) / 64)),
-                           dim3(1024), 0, st, static_cast<const float *>(workspace),
-                           ste_workgroups(T), (int)d, grad_gamma);
+        const int64_t P = ste_workgroups(T);
+        // P d floats keep the slices 8-byte aligned (d % 8 == 0)
+        double *slice = reinterpret_cast<double *>(static_cast<float *>(workspace) + P * d);
+        hipLaunchKernelGGL(mxb::ggamma_slice_kernel,
+                           dim3((unsigned)((d + 63) / 64), (unsigned)mxb::GG_SLICES), dim3(256), 0,
+                           st, static_cast<const float *>(workspace), P, (int)d, slice);
         e = hipGetLastError();
+        if (e == hipSuccess) {
+            hipLaunchKernelGGL(mxb::ggamma_final_kernel, dim3((unsigned)((d + 255) / 256)),
+                               dim3(256), 0, st, static_cast<const double *>(slice), (int)d,
+                               grad_gamma);
+            e = hipGetLastError();
+        }
     }
     if (e != hipSuccess)
         return mxk::fail(MX_EHIP, "kernel launch failed: %s", hipGetErrorString(e));

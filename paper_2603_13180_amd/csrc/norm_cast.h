@@ -283,6 +283,17 @@ __device__ __forceinline__ double readlane_f64(double v, int lane)
     return __builtin_bit_cast(double, ((unsigned long long)hi << 32) | lo);
 }
 
+// Workgroup barrier that orders LDS accesses only.  The threads of these
+// kernels share data through LDS alone, and __syncthreads()' fence would also
+// wait for every global load and store in flight, including loads issued
+// ahead for later rows and the stores of the row just finished.
+__device__ __forceinline__ void lds_barrier()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // Sum of one double per lane over a team of TL lanes; every lane of the team
 // gets the same bits.  Inside a 16-lane row: DPP quad permutes (lane i^1,
 // i^2) and the half-row and row mirrors, each step adding the same two values
@@ -314,7 +325,7 @@ __device__ __forceinline__ double team_sum(double s, double *red, int tid)
         const int wave = tid >> 6;
         if ((tid & 63) == 0)
             red[wave] = s;
-        __syncthreads();
+        lds_barrier();
         const int first = (wave / NW) * NW;
         double t = 0.0;
 #pragma unroll
@@ -436,7 +447,7 @@ norm_cast_kernel(Args A)
         six_sg = A.six_sg;
         rcp_six_sg = A.rcp_six_sg;
         six_sg_ok = six_sg >= 0x1p-90f;
-        __syncthreads();
+        lds_barrier();
     }
 
     const int tid = threadIdx.x;
@@ -660,7 +671,7 @@ norm_cast_kernel(Args A)
 
         // ---- the row's K scale bytes: LDS -> one wide store per lane ----
         if constexpr (TL > 64) {
-            __syncthreads();
+            lds_barrier();
         } else {
             // the team lives in one wave: order its LDS writes before the reads
             __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
