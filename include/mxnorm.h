@@ -221,8 +221,8 @@ mx_status mx_matmul_fwd(const uint8_t *a_codes, const uint8_t *a_scales, const u
  * = X and rho = rho~ this is MXCast(rho~ . X) blocked along tokens; with rho
  * NULL it gives MXCast(grad_H^T) and the weight blocked along its output
  * dimension.  block: 32 (else MX_EUNSUPPORTED).  R a multiple of 32 and C of
- * 8 (else MX_EINVAL); x and codes 16-byte aligned, rho 4-byte.  R == 0 is a
- * no-op.
+ * 8 (else MX_EINVAL); R <= 2^31 and C <= 2^23 (else MX_EUNSUPPORTED); x and
+ * codes 16-byte aligned, rho 4-byte.  R == 0 is a no-op.
  */
 mx_status mx_cast_t_fwd(const void *x, const float *rho, int64_t R, int64_t C, int block,
                         int elem, int scale_mode, uint8_t *codes, uint8_t *scales, void *stream);

@@ -51,19 +51,27 @@ struct CastTArgs {
 
 // Workgroup (span, tile_c) casts columns [64 tile_c, +64) over a span of
 // `tiles` x 128 rows, 128 rows at a time (the host sizes the span so that
-// the grid still fills the chip).  Each 128 x 64 tile is staged in
-// LDS as it is in x (128 bytes per row; the next tile's loads are already in
-// flight in registers); wave w then casts rows 32w .. 32w+31 of it, lane c
-// column c: it reads its 32 values down the column (the 64 lanes of a read
-// on 128 consecutive bytes: no bank conflicts), scales them by rho, decides
-// the E8M0 byte from their absmax and writes 32 codes (E4M3: 32 B; E2M1:
-// 16 B) into row c0 + c of the transposed output.  The span's 64 scale bytes
-// per column are gathered in LDS and written at the end, 64 contiguous
-// bytes per output row, rather than one scattered byte per tile.
+// the grid still fills the chip).  Each 128 x 64 tile is staged in LDS as it
+// is in x (128 bytes per row, 32 bytes of padding after every 32 rows; the
+// next tile's loads are already in flight in registers).  Wave w then casts
+// columns 16w .. 16w+15: lane 4 cc + b takes column 16w + cc over rows
+// 32b .. 32b+31 (one scale block), reads its 32 values down the column,
+// scales them by rho, decides the E8M0 byte from their absmax and writes 32
+// codes (E4M3: 32 B; E2M1: 16 B) into row c0 + 16w + cc of the transposed
+// output.  The four lanes of a column write 128 (E4M3) or 64 (E2M1)
+// contiguous bytes, so a store instruction covers whole cache lines of 16
+// output rows.  With the padding, the 64 lanes of a read fall in distinct
+// LDS banks (the blocks sit 8 banks apart).  The span's scale bytes per
+// column are gathered in LDS and written at the end, 64 contiguous bytes
+// per output row, rather than one scattered byte per tile.
+constexpr int CT_PITCH = CT_COLS * 2;           // bytes per staged row
+constexpr int CT_BLKB = 32 * CT_PITCH + 32;     // bytes per staged 32-row block
+__device__ __forceinline__ int ct_off(int r) { return (r >> 5) * CT_BLKB + (r & 31) * CT_PITCH; }
+
 template <bool FP4>
 __global__ void __launch_bounds__(256) cast_t_kernel(CastTArgs A)
 {
-    __shared__ __attribute__((aligned(16))) uint16_t tile[CT_ROWS * CT_COLS];
+    __shared__ __attribute__((aligned(16))) uint8_t tile[4 * CT_BLKB];
     __shared__ float rs[CT_ROWS];
     __shared__ __attribute__((aligned(16))) uint8_t sb[CT_COLS][CT_TILES * 4];
 
@@ -71,51 +79,71 @@ __global__ void __launch_bounds__(256) cast_t_kernel(CastTArgs A)
     const int64_t span0 = (int64_t)blockIdx.y * CT_ROWS * A.tiles;
     const int64_t c0 = (int64_t)blockIdx.x * CT_COLS;
     const int ntiles = (int)min((int64_t)A.tiles, (A.R - span0 + CT_ROWS - 1) / CT_ROWS);
-    const int w = tid >> 6, c = tid & 63;
-    const int64_t orow = c0 + c;
+    const int w = tid >> 6, lane = tid & 63;
+    const int cc = 16 * w + (lane >> 2), blk = lane & 3; // column in the tile, 32-row block
+    const int64_t orow = c0 + cc;
     const bool col_ok = orow < A.C;
 
-    // staging: thread t moves 16-byte chunk t % 8 of tile rows t / 8 + 32 k
+    // staging: thread t moves 16-byte chunk t % 8 of tile rows t / 8 + 32 k,
+    // through a buffer resource over the tile's rows (chunks past C and rows
+    // past R read zeros; no per-lane branch, which would serialise the loads)
     const int ch = tid & 7;
-    const bool chunk_ok = c0 + 8 * ch < A.C; // C % 8 == 0: whole chunks
-    auto fetch = [&](int64_t r0, uint4 v[4]) {
+    const uint32_t chunk_off = c0 + 8 * ch < A.C ? 16u * (uint32_t)ch : kOutside; // C % 8 == 0
+    const uint32_t pitch = (uint32_t)A.C * 2u;
+    // the tile's rho values travel with its rows (thread t < 128: row t), so
+    // that waiting for them is not a wait for every store in flight
+    auto fetch = [&](int64_t r0, uint4 v[4], float &rv) {
+        const uint32_t rows = (uint32_t)max((int64_t)0, min((int64_t)CT_ROWS, A.R - r0));
+        const __amdgpu_buffer_rsrc_t xr = buffer_rsrc(A.x + r0 * A.C + c0, rows * pitch);
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-            const int r = (tid >> 3) + 32 * k;
-            v[k] = (chunk_ok && r0 + r < A.R)
-                       ? load_stream(reinterpret_cast<const uint4 *>(A.x + (r0 + r) * A.C + c0) + ch)
-                       : make_uint4(0u, 0u, 0u, 0u);
+            const uint32_t r = (uint32_t)((tid >> 3) + 32 * k);
+            const uint32_t off = chunk_off == kOutside ? kOutside : r * pitch + chunk_off;
+            const u32x4_t t = __builtin_amdgcn_raw_buffer_load_b128(xr, (int)off, 0, kBufNT);
+            v[k] = make_uint4(t.x, t.y, t.z, t.w);
+        }
+        if (A.rho) {
+            const __amdgpu_buffer_rsrc_t rr = buffer_rsrc(A.rho + r0, rows * 4u);
+            rv = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                               rr, (int)(tid < CT_ROWS ? 4u * (uint32_t)tid : kOutside), 0, 0));
+        } else {
+            rv = 1.0f;
         }
     };
     uint4 nxt[4];
-    fetch(span0, nxt);
+    float nrho;
+    fetch(span0, nxt, nrho);
 
     for (int t = 0; t < ntiles; ++t) {
         const int64_t r0 = span0 + (int64_t)t * CT_ROWS;
 #pragma unroll
         for (int k = 0; k < 4; ++k)
-            *reinterpret_cast<uint4 *>(&tile[((tid >> 3) + 32 * k) * CT_COLS + 8 * ch]) = nxt[k];
+            *reinterpret_cast<uint4 *>(&tile[ct_off((tid >> 3) + 32 * k) + 16 * ch]) = nxt[k];
         if (tid < CT_ROWS)
-            rs[tid] = (A.rho && r0 + tid < A.R) ? A.rho[r0 + tid] : 1.0f;
+            rs[tid] = nrho;
         lds_barrier();
         if (t + 1 < ntiles)
-            fetch(r0 + CT_ROWS, nxt);
+            fetch(r0 + CT_ROWS, nxt, nrho);
 
-        const int64_t rb = r0 + 32 * w; // first row of this wave's block
+        const int64_t rb = r0 + 32 * blk; // first row of this lane's block
         if (rb < A.R && col_ok) {
-            // pass 1: the block absmax of the scaled values (integer max of
-            // the magnitude bits: NaN propagates); pass 2 re-reads the column
-            // from LDS and converts a few values at a time
-            const uint16_t *col = tile + 32 * w * CT_COLS + c;
-            const float *rr = rs + 32 * w;
-            auto value = [&](int i) {
-                const float v = __uint_as_float((uint32_t)col[i * CT_COLS] << 16);
-                return A.rho ? v * rr[i] : v;
+            // the block's 32 scaled values, read once from LDS and kept in
+            // registers; their absmax as the integer max of the magnitude
+            // bits (NaN propagates)
+            const uint8_t *col = tile + blk * CT_BLKB + 2 * cc;
+            const float *rr = rs + 32 * blk;
+            auto bits = [&](int i) {
+                return (uint32_t)*reinterpret_cast<const uint16_t *>(col + i * CT_PITCH);
             };
+            float tv[32];
             uint32_t m = 0;
-#pragma unroll 8
-            for (int i = 0; i < 32; ++i)
-                m = max(m, __float_as_uint(value(i)) & 0x7FFFFFFFu);
+#pragma unroll
+            for (int i = 0; i < 32; ++i) {
+                const float v = __uint_as_float(bits(i) << 16);
+                tv[i] = A.rho ? v * rr[i] : v;
+                m = max(m, __float_as_uint(tv[i]) & 0x7FFFFFFFu);
+            }
+            auto value = [&](int i) { return tv[i]; };
             const float a = __uint_as_float(m);
             uint32_t byte;
             if constexpr (!FP4) {
@@ -138,7 +166,7 @@ __global__ void __launch_bounds__(256) cast_t_kernel(CastTArgs A)
                         uint32_t r = 0x7F7F7F7Fu;
 #pragma unroll
                         for (int e = 0; e < 4; ++e)
-                            r |= ((uint32_t)col[(4 * k + e) * CT_COLS] >> 15) << (8 * e + 7);
+                            r |= (bits(4 * k + e) >> 15) << (8 * e + 7);
                         q[k] = r;
                     }
                 }
@@ -162,14 +190,14 @@ __global__ void __launch_bounds__(256) cast_t_kernel(CastTArgs A)
                         p = 0x77777777u;
 #pragma unroll
                         for (int e = 0; e < 8; ++e)
-                            p |= ((uint32_t)col[(8 * k + e) * CT_COLS] >> 15) << (4 * e + 3);
+                            p |= (bits(8 * k + e) >> 15) << (4 * e + 3);
                     }
                     q[k] = p;
                 }
                 *reinterpret_cast<uint4 *>(A.codes + orow * (A.R / 2) + rb / 2) =
                     make_uint4(q[0], q[1], q[2], q[3]);
             }
-            sb[c][4 * t + w] = (uint8_t)byte;
+            sb[cc][4 * t + blk] = (uint8_t)byte;
         }
         lds_barrier(); // the tile is overwritten next
     }
@@ -178,16 +206,16 @@ __global__ void __launch_bounds__(256) cast_t_kernel(CastTArgs A)
     // inside the span), written by the 4 threads of its row as 16-byte pieces
     // when whole and aligned, else byte by byte
     const int64_t nblk = min((int64_t)ntiles * 4, (A.R - span0) / 32);
-    const int cc = tid >> 2, part = tid & 3;
-    const int64_t srow = c0 + cc;
+    const int sc = tid >> 2, part = tid & 3;
+    const int64_t srow = c0 + sc;
     if (srow < A.C) {
         uint8_t *dst = A.scales + srow * (A.R / 32) + span0 / 32;
         const int lo = 16 * part;
         if (lo + 16 <= nblk && (((uintptr_t)(dst + lo)) & 15) == 0) {
-            *reinterpret_cast<uint4 *>(dst + lo) = *reinterpret_cast<const uint4 *>(&sb[cc][lo]);
+            *reinterpret_cast<uint4 *>(dst + lo) = *reinterpret_cast<const uint4 *>(&sb[sc][lo]);
         } else {
             for (int k = lo; k < lo + 16 && k < nblk; ++k)
-                dst[k] = sb[cc][k];
+                dst[k] = sb[sc][k];
         }
     }
 }
@@ -525,8 +553,8 @@ mx_status mx_cast_t_fwd(const void *x, const float *rho, int64_t R, int64_t C, i
         return mxk::fail(MX_EINVAL, "R must be a multiple of the block (32)");
     if (C % 8 != 0)
         return mxk::fail(MX_EINVAL, "C must be a multiple of 8");
-    if (R > ((int64_t)1 << 31) || C > ((int64_t)1 << 31))
-        return mxk::fail(MX_EUNSUPPORTED, "matrix too large");
+    if (R > ((int64_t)1 << 31) || C > ((int64_t)1 << 23))
+        return mxk::fail(MX_EUNSUPPORTED, "matrix too large (R <= 2^31, C <= 2^23)");
     if (R == 0)
         return MX_OK;
     if (!x || !codes || !scales)
@@ -541,12 +569,12 @@ mx_status mx_cast_t_fwd(const void *x, const float *rho, int64_t R, int64_t C, i
     A.R = R;
     A.C = C;
     A.mode = scale_mode;
-    // tiles per workgroup: as many as keep about 1024 workgroups (longer
+    // tiles per workgroup: as many as keep about 2048 workgroups (longer
     // spans write longer runs of scale bytes), at most CT_TILES
     const int64_t col_tiles = (C + mxb::CT_COLS - 1) / mxb::CT_COLS;
     const int64_t row_tiles = (R + mxb::CT_ROWS - 1) / mxb::CT_ROWS;
     A.tiles = (int)std::max<int64_t>(1, std::min<int64_t>(mxb::CT_TILES,
-                                                          col_tiles * row_tiles / 1024));
+                                                          col_tiles * row_tiles / 2048));
     const int64_t span = (int64_t)mxb::CT_ROWS * A.tiles;
     const dim3 grid((unsigned)col_tiles, (unsigned)((R + span - 1) / span));
     if (grid.y > 65535u)
