@@ -72,7 +72,7 @@ template <bool FP4>
 __global__ void __launch_bounds__(256) cast_t_kernel(CastTArgs A)
 {
     __shared__ __attribute__((aligned(16))) uint8_t tile[4 * CT_BLKB];
-    __shared__ float rs[CT_ROWS];
+    __shared__ __attribute__((aligned(16))) float rs[CT_ROWS];
     __shared__ __attribute__((aligned(16))) uint8_t sb[CT_COLS][CT_TILES * 4];
 
     const int tid = threadIdx.x;
@@ -138,10 +138,17 @@ __global__ void __launch_bounds__(256) cast_t_kernel(CastTArgs A)
             float tv[32];
             uint32_t m = 0;
 #pragma unroll
-            for (int i = 0; i < 32; ++i) {
-                const float v = __uint_as_float(bits(i) << 16);
-                tv[i] = A.rho ? v * rr[i] : v;
-                m = max(m, __float_as_uint(tv[i]) & 0x7FFFFFFFu);
+            for (int k = 0; k < 8; ++k) {
+                // four rho values per 16-byte read (the block's lanes share it)
+                const float4 r4 = A.rho ? reinterpret_cast<const float4 *>(rr)[k]
+                                        : make_float4(1.0f, 1.0f, 1.0f, 1.0f);
+                const float rk[4] = {r4.x, r4.y, r4.z, r4.w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float v = __uint_as_float(bits(4 * k + e) << 16);
+                    tv[4 * k + e] = A.rho ? v * rk[e] : v;
+                    m = max(m, __float_as_uint(tv[4 * k + e]) & 0x7FFFFFFFu);
+                }
             }
             auto value = [&](int i) { return tv[i]; };
             const float a = __uint_as_float(m);
