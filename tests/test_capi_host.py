@@ -205,6 +205,7 @@ def test_mx_matmul_rejects_bad_arguments(args, status):
     (dict(R=-1), 1), (dict(C=0), 1), (dict(elem=2), 1), (dict(mode=3), 1), (dict(block=16), 2),
     (dict(R=48), 1), (dict(C=12), 1), (dict(x=None), 1), (dict(codes=None), 1), (dict(x=A8), 1),
     (dict(rho=OUT + 2), 1), (dict(R=0, x=None, codes=None, scales=None), 0),
+    (dict(C=(1 << 23) + 8), 2), (dict(R=(1 << 31) + 32), 2),
 ])
 def test_mx_cast_t_rejects_bad_arguments(args, status):
     lib = mxnorm.load()

@@ -74,6 +74,33 @@ def test_cast_t_edge_columns(elem):
             check_cast_t(xb, rho, elem, mode)
 
 
+@pytest.mark.parametrize("elem", ["e4m3", "e2m1"])
+@pytest.mark.parametrize("R,C", [(16384, 4096), (32768, 4096), (4096, 28672)])
+def test_cast_t_multi_tile_spans_sampled(elem, R, C):
+    """Shapes where a workgroup walks several 128-row tiles (up to 8; the
+    bench's [32768, 4096] and the wide grad_H of the gate+up projection):
+    output rows of sampled columns -- the first and last of column tiles and
+    random ones -- against the oracle's cast of those columns alone (an
+    output row depends only on its column and rho)."""
+    rng = np.random.default_rng(R + C)
+    xb = synth.gaussian(R, C, seed=C, scale=3.0)
+    rho = rng.uniform(0.01, 8.0, R).astype(np.float32)
+    cols = np.unique(np.concatenate([[0, 1, 63, 64, 127, C - 64, C - 1],
+                                     rng.choice(C, 24, replace=False)]))
+    x = dev_bf16(xb)
+    codes, scales = mxnorm.mx_cast_t_fwd(x, torch.from_numpy(rho).to(DEV), elem=elem)
+    torch.cuda.synchronize()
+    c, sc = codes.cpu().numpy(), scales.cpu().numpy()
+    # the oracle casts a column block of 8 (its C must be a multiple of 8)
+    for c0 in np.unique(cols // 8 * 8):
+        wc, ws = oracle.mxcast_t(np.ascontiguousarray(xb[:, c0:c0 + 8]), rho, B=32, elem=elem,
+                                 mode="rceil")
+        assert np.array_equal(sc[c0:c0 + 8], ws), "cast_t [%d, %d] %s scales, cols %d.." % (
+            R, C, elem, c0)
+        assert np.array_equal(c[c0:c0 + 8], wc), "cast_t [%d, %d] %s codes, cols %d.." % (
+            R, C, elem, c0)
+
+
 def test_cast_t_empty():
     x = torch.empty(0, 64, dtype=torch.bfloat16, device=DEV)
     c, s = mxnorm.mx_cast_t_fwd(x)
@@ -131,7 +158,7 @@ def check_ste(T, d, gamma, out_dtype, want_gg, seed=0, xb=None):
 
 
 @pytest.mark.parametrize("T,d", [(1, 8), (33, 64), (100, 1024), (40, 4096), (65, 2048),
-                                 (9, 10240), (3, 32768), (70, 2056)])
+                                 (9, 10240), (3, 32768), (70, 2056), (2049, 256), (4100, 512)])
 def test_ste_shapes(T, d):
     check_ste(T, d, True, torch.bfloat16, True)
     check_ste(T, d, False, torch.float32, True)
