@@ -139,14 +139,15 @@ __global__ void __launch_bounds__(256) cast_t_kernel(CastTArgs A)
             uint32_t m = 0;
 #pragma unroll
             for (int k = 0; k < 8; ++k) {
-                // four rho values per 16-byte read (the block's lanes share it)
-                const float4 r4 = A.rho ? reinterpret_cast<const float4 *>(rr)[k]
-                                        : make_float4(1.0f, 1.0f, 1.0f, 1.0f);
+                // four rho values per 16-byte read (the block's lanes share
+                // it); without rho the staged values are 1 and t = RN(x * 1)
+                // = x, so the reads need no branch
+                const float4 r4 = reinterpret_cast<const float4 *>(rr)[k];
                 const float rk[4] = {r4.x, r4.y, r4.z, r4.w};
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     const float v = __uint_as_float(bits(4 * k + e) << 16);
-                    tv[4 * k + e] = A.rho ? v * rk[e] : v;
+                    tv[4 * k + e] = v * rk[e];
                     m = max(m, __float_as_uint(tv[4 * k + e]) & 0x7FFFFFFFu);
                 }
             }
@@ -155,26 +156,29 @@ __global__ void __launch_bounds__(256) cast_t_kernel(CastTArgs A)
             uint32_t byte;
             if constexpr (!FP4) {
                 byte = e8m0_byte<false>(a, A.mode);
-                // FLOOR: |t| <= 448 * 2^e, saturate before the conversion
-                // (RCEIL never exceeds it)
-                const float lim = A.mode == MX_SCALE_FLOOR
-                                      ? __uint_as_float(((byte + 8u) << 23) | 0x600000u)
-                                      : __builtin_inff();
+                if (A.mode == MX_SCALE_FLOOR) {
+                    // |t| <= 448 * 2^e: saturate before the conversion
+                    // (RCEIL never exceeds it)
+                    const float lim = __uint_as_float(((byte + 8u) << 23) | 0x600000u);
+#pragma unroll
+                    for (int i = 0; i < 32; ++i)
+                        tv[i] = __builtin_amdgcn_fmed3f(tv[i], -lim, lim);
+                }
                 const float scale = __uint_as_float(byte << 23);
                 uint32_t q[8];
 #pragma unroll
-                for (int k = 0; k < 8; ++k) {
-                    float v[4];
+                for (int k = 0; k < 8; ++k)
+                    q[k] = e4m3x4_hw(value(4 * k), value(4 * k + 1), value(4 * k + 2), value(4 * k + 3), scale);
+                if (__builtin_amdgcn_ballot_w64(byte == 0xFFu)) { // rare: non-finite input
+                    if (byte == 0xFFu) { // input signs, all-ones magnitude
 #pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        v[e] = __builtin_amdgcn_fmed3f(value(4 * k + e), -lim, lim);
-                    q[k] = e4m3x4_hw(v[0], v[1], v[2], v[3], scale);
-                    if (byte == 0xFFu) { // non-finite input: input signs, all-ones magnitude
-                        uint32_t r = 0x7F7F7F7Fu;
+                        for (int k = 0; k < 8; ++k) {
+                            uint32_t r = 0x7F7F7F7Fu;
 #pragma unroll
-                        for (int e = 0; e < 4; ++e)
-                            r |= (bits(4 * k + e) >> 15) << (8 * e + 7);
-                        q[k] = r;
+                            for (int e = 0; e < 4; ++e)
+                                r |= (bits(4 * k + e) >> 15) << (8 * e + 7);
+                            q[k] = r;
+                        }
                     }
                 }
                 uint4 *dst = reinterpret_cast<uint4 *>(A.codes + orow * A.R + rb);
@@ -193,13 +197,19 @@ __global__ void __launch_bounds__(256) cast_t_kernel(CastTArgs A)
                     p = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(p, value(8 * k + 2), value(8 * k + 3), scale, 1);
                     p = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(p, value(8 * k + 4), value(8 * k + 5), scale, 2);
                     p = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(p, value(8 * k + 6), value(8 * k + 7), scale, 3);
-                    if (byte == 0xFFu) {
-                        p = 0x77777777u;
-#pragma unroll
-                        for (int e = 0; e < 8; ++e)
-                            p |= (bits(8 * k + e) >> 15) << (4 * e + 3);
-                    }
                     q[k] = p;
+                }
+                if (__builtin_amdgcn_ballot_w64(byte == 0xFFu)) { // rare: non-finite input
+                    if (byte == 0xFFu) {
+#pragma unroll
+                        for (int k = 0; k < 4; ++k) {
+                            uint32_t p = 0x77777777u;
+#pragma unroll
+                            for (int e = 0; e < 8; ++e)
+                                p |= (bits(8 * k + e) >> 15) << (4 * e + 3);
+                            q[k] = p;
+                        }
+                    }
                 }
                 *reinterpret_cast<uint4 *>(A.codes + orow * (A.R / 2) + rb / 2) =
                     make_uint4(q[0], q[1], q[2], q[3]);
