@@ -560,19 +560,20 @@ def main():
     copy_gbps = 2 * x0.numel() * 2 / (m * 1e-3) / 1e9
 
     # the backward's streaming kernels at the same shape: the STE (x and a
-    # synthetic grad_Z in rotation) and the column cast of rho~ X
+    # synthetic grad_Z) and the column cast of rho~ X, inputs and outputs in
+    # rotation like the forward's
     gzs = [torch.randn(T, d, device=dev).to(torch.bfloat16) for _ in range(n_sets)]
-    gxo = torch.empty(T, d, dtype=torch.bfloat16, device=dev)
+    gxo = [torch.empty(T, d, dtype=torch.bfloat16, device=dev) for _ in range(n_sets)]
     ggo = torch.empty(d, dtype=torch.float32, device=dev)
     wsp = torch.empty(mxnorm.load().mxnorm_ste_bwd_workspace_bytes(T, d), dtype=torch.uint8,
                       device=dev)
-    tc = torch.empty(d, T, dtype=torch.uint8, device=dev)
-    ts = torch.empty(d, T // 32, dtype=torch.uint8, device=dev)
+    tc = [torch.empty(d, T, dtype=torch.uint8, device=dev) for _ in range(n_sets)]
+    ts = [torch.empty(d, T // 32, dtype=torch.uint8, device=dev) for _ in range(n_sets)]
     ms_ste = time_launches(lambda i: mxnorm.mxnorm_ste_bwd(
-        xs[i], gzs[i], g, rho[i], grad_x=gxo, grad_gamma=ggo, workspace=wsp),
-        n_sets, 50, 5, stream)
-    ms_ct = time_launches(lambda i: mxnorm.mx_cast_t_fwd(xs[i], rho[i], codes=tc, scales=ts),
-                          n_sets, 50, 5, stream)
+        xs[i], gzs[i], g, rho[i], grad_x=gxo[i], grad_gamma=ggo, workspace=wsp),
+        n_sets, 60, 30, stream)
+    ms_ct = time_launches(lambda i: mxnorm.mx_cast_t_fwd(xs[i], rho[i], codes=tc[i], scales=ts[i]),
+                          n_sets, 60, 30, stream)
     bwd = {"ste_bwd": {"us": round(ms_ste * 1e3, 2),
                        "GB/s": round(ste_bytes(T, d) / (ms_ste * 1e-3) / 1e9, 1)},
            "cast_t_rho_x_mxfp8": {"us": round(ms_ct * 1e3, 2),

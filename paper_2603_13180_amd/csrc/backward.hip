@@ -35,9 +35,12 @@ using namespace mxk;
 
 // ---------------------------------------------------------- column cast --
 
-constexpr int CT_ROWS = 128; // tile rows (4 waves x one 32-row block)
-constexpr int CT_COLS = 64;  // tile columns (one per lane)
-constexpr int CT_TILES = 16; // most tiles per workgroup (a span of up to 2048 rows)
+constexpr int CT_ROWS = 128;  // tile rows (four 32-row blocks)
+constexpr int CT_COLS = 128;  // tile columns (64 per pass of the 256 threads)
+constexpr int CT_TILES = 16;  // most tiles per workgroup (a span of up to 2048 rows)
+constexpr int CT_CPR = CT_COLS / 8;       // 16-byte chunks per tile row
+constexpr int CT_RPP = 256 / CT_CPR;      // tile rows per staging pass
+constexpr int CT_NLD = CT_ROWS / CT_RPP;  // staging loads per thread
 
 struct CastTArgs {
     const uint16_t *x;
@@ -49,21 +52,24 @@ struct CastTArgs {
     int tiles; // tiles per span, 1 .. CT_TILES
 };
 
-// Workgroup (span, tile_c) casts columns [64 tile_c, +64) over a span of
+// Workgroup (span, tile_c) casts columns [128 tile_c, +128) over a span of
 // `tiles` x 128 rows, 128 rows at a time (the host sizes the span so that
-// the grid still fills the chip).  Each 128 x 64 tile is staged in LDS as it
-// is in x (128 bytes per row, 32 bytes of padding after every 32 rows; the
-// next tile's loads are already in flight in registers).  Wave w then casts
-// columns 16w .. 16w+15: lane 4 cc + b takes column 16w + cc over rows
-// 32b .. 32b+31 (one scale block), reads its 32 values down the column,
-// scales them by rho, decides the E8M0 byte from their absmax and writes 32
-// codes (E4M3: 32 B; E2M1: 16 B) into row c0 + 16w + cc of the transposed
-// output.  The four lanes of a column write 128 (E4M3) or 64 (E2M1)
-// contiguous bytes, so a store instruction covers whole cache lines of 16
-// output rows.  With the padding, the 64 lanes of a read fall in distinct
-// LDS banks (the blocks sit 8 banks apart).  The span's scale bytes per
-// column are gathered in LDS and written at the end, 64 contiguous bytes
-// per output row, rather than one scattered byte per tile.
+// the grid still fills the chip).  Each 128 x 128 tile is staged in LDS as
+// it is in x (256 bytes per row, 32 bytes of padding after every 32 rows;
+// the next tile's loads are already in flight in registers).  The 256-byte
+// row pieces read from x are what sets the tile width: a transposing stream
+// with 128-byte pieces runs ~12% slower.  The tile is cast in two passes of
+// 64 columns; in pass h wave w casts columns 64h + 16w .. +15: lane 4 cc + b
+// takes column 64h + 16w + cc over rows 32b .. 32b+31 (one scale block),
+// reads its 32 values down the column, scales them by rho, decides the E8M0
+// byte from their absmax and writes 32 codes (E4M3: 32 B; E2M1: 16 B) into
+// that column's row of the transposed output.  The four lanes of a column
+// write 128 (E4M3) or 64 (E2M1) contiguous bytes, so a store instruction
+// covers whole cache lines of 16 output rows.  With the padding, the 64
+// lanes of a read fall in distinct LDS banks (the blocks sit 8 banks
+// apart).  The span's scale bytes per column are gathered in LDS and
+// written at the end, 64 contiguous bytes per output row, rather than one
+// scattered byte per tile.
 constexpr int CT_PITCH = CT_COLS * 2;           // bytes per staged row
 constexpr int CT_BLKB = 32 * CT_PITCH + 32;     // bytes per staged 32-row block
 __device__ __forceinline__ int ct_off(int r) { return (r >> 5) * CT_BLKB + (r & 31) * CT_PITCH; }
@@ -80,24 +86,23 @@ __global__ void __launch_bounds__(256) cast_t_kernel(CastTArgs A)
     const int64_t c0 = (int64_t)blockIdx.x * CT_COLS;
     const int ntiles = (int)min((int64_t)A.tiles, (A.R - span0 + CT_ROWS - 1) / CT_ROWS);
     const int w = tid >> 6, lane = tid & 63;
-    const int cc = 16 * w + (lane >> 2), blk = lane & 3; // column in the tile, 32-row block
-    const int64_t orow = c0 + cc;
-    const bool col_ok = orow < A.C;
+    const int blk = lane & 3; // 32-row block this lane casts
 
-    // staging: thread t moves 16-byte chunk t % 8 of tile rows t / 8 + 32 k,
-    // through a buffer resource over the tile's rows (chunks past C and rows
-    // past R read zeros; no per-lane branch, which would serialise the loads)
-    const int ch = tid & 7;
+    // staging: thread t moves 16-byte chunk t % CT_CPR of tile rows
+    // t / CT_CPR + CT_RPP k, through a buffer resource over the tile's rows
+    // (chunks past C and rows past R read zeros; no per-lane branch, which
+    // would serialise the loads)
+    const int ch = tid % CT_CPR, rbase = tid / CT_CPR;
     const uint32_t chunk_off = c0 + 8 * ch < A.C ? 16u * (uint32_t)ch : kOutside; // C % 8 == 0
     const uint32_t pitch = (uint32_t)A.C * 2u;
     // the tile's rho values travel with its rows (thread t < 128: row t), so
     // that waiting for them is not a wait for every store in flight
-    auto fetch = [&](int64_t r0, uint4 v[4], float &rv) {
+    auto fetch = [&](int64_t r0, uint4 v[CT_NLD], float &rv) {
         const uint32_t rows = (uint32_t)max((int64_t)0, min((int64_t)CT_ROWS, A.R - r0));
         const __amdgpu_buffer_rsrc_t xr = buffer_rsrc(A.x + r0 * A.C + c0, rows * pitch);
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const uint32_t r = (uint32_t)((tid >> 3) + 32 * k);
+        for (int k = 0; k < CT_NLD; ++k) {
+            const uint32_t r = (uint32_t)(rbase + CT_RPP * k);
             const uint32_t off = chunk_off == kOutside ? kOutside : r * pitch + chunk_off;
             const u32x4_t t = __builtin_amdgcn_raw_buffer_load_b128(xr, (int)off, 0, kBufNT);
             v[k] = make_uint4(t.x, t.y, t.z, t.w);
@@ -110,15 +115,15 @@ __global__ void __launch_bounds__(256) cast_t_kernel(CastTArgs A)
             rv = 1.0f;
         }
     };
-    uint4 nxt[4];
+    uint4 nxt[CT_NLD];
     float nrho;
     fetch(span0, nxt, nrho);
 
     for (int t = 0; t < ntiles; ++t) {
         const int64_t r0 = span0 + (int64_t)t * CT_ROWS;
 #pragma unroll
-        for (int k = 0; k < 4; ++k)
-            *reinterpret_cast<uint4 *>(&tile[ct_off((tid >> 3) + 32 * k) + 16 * ch]) = nxt[k];
+        for (int k = 0; k < CT_NLD; ++k)
+            *reinterpret_cast<uint4 *>(&tile[ct_off(rbase + CT_RPP * k) + 16 * ch]) = nxt[k];
         if (tid < CT_ROWS)
             rs[tid] = nrho;
         lds_barrier();
@@ -126,7 +131,11 @@ __global__ void __launch_bounds__(256) cast_t_kernel(CastTArgs A)
             fetch(r0 + CT_ROWS, nxt, nrho);
 
         const int64_t rb = r0 + 32 * blk; // first row of this lane's block
-        if (rb < A.R && col_ok) {
+#pragma unroll
+        for (int h = 0; h < CT_COLS / 64; ++h) {
+        const int cc = 64 * h + 16 * w + (lane >> 2); // column in the tile
+        const int64_t orow = c0 + cc;
+        if (rb < A.R && orow < A.C) {
             // the block's 32 scaled values, read once from LDS and kept in
             // registers; their absmax as the integer max of the magnitude
             // bits (NaN propagates)
@@ -216,23 +225,27 @@ __global__ void __launch_bounds__(256) cast_t_kernel(CastTArgs A)
             }
             sb[cc][4 * t + blk] = (uint8_t)byte;
         }
+        }
         lds_barrier(); // the tile is overwritten next
     }
 
     // the span's scale bytes: column c has 4 per tile (fewer where R ends
-    // inside the span), written by the 4 threads of its row as 16-byte pieces
-    // when whole and aligned, else byte by byte
+    // inside the span), written as four 16-byte pieces per output row when
+    // whole and aligned, else byte by byte
     const int64_t nblk = min((int64_t)ntiles * 4, (A.R - span0) / 32);
-    const int sc = tid >> 2, part = tid & 3;
-    const int64_t srow = c0 + sc;
-    if (srow < A.C) {
-        uint8_t *dst = A.scales + srow * (A.R / 32) + span0 / 32;
-        const int lo = 16 * part;
-        if (lo + 16 <= nblk && (((uintptr_t)(dst + lo)) & 15) == 0) {
-            *reinterpret_cast<uint4 *>(dst + lo) = *reinterpret_cast<const uint4 *>(&sb[sc][lo]);
-        } else {
-            for (int k = lo; k < lo + 16 && k < nblk; ++k)
-                dst[k] = sb[sc][k];
+#pragma unroll
+    for (int pc = tid; pc < CT_COLS * 4; pc += 256) {
+        const int sc = pc >> 2, part = pc & 3;
+        const int64_t srow = c0 + sc;
+        if (srow < A.C) {
+            uint8_t *dst = A.scales + srow * (A.R / 32) + span0 / 32;
+            const int lo = 16 * part;
+            if (lo + 16 <= nblk && (((uintptr_t)(dst + lo)) & 15) == 0) {
+                *reinterpret_cast<uint4 *>(dst + lo) = *reinterpret_cast<const uint4 *>(&sb[sc][lo]);
+            } else {
+                for (int k = lo; k < lo + 16 && k < nblk; ++k)
+                    dst[k] = sb[sc][k];
+            }
         }
     }
 }
