@@ -2,7 +2,9 @@
 
 Each check ties the oracle to something outside itself: the formats' published
 properties (bias, largest finite value, NaN encoding), PyTorch's independent
-float8_e4m3fn conversion, the RCEIL rule as implemented with an fp32 division
+float8_e4m3fn conversion (on every fp32 value of the range that matters), a
+round-to-nearest-even definition of E2M1 by midpoint counting (likewise on
+every fp32 value of its range), the RCEIL rule as implemented with an fp32 division
 and a ceil-of-log2 on the exponent bits (the MXFP8 recipe the paper's
 experiments use, Sec. 3.2), and hand-listed E2M1 rounding boundaries.
 """
@@ -89,6 +91,21 @@ def test_e4m3_encode_matches_torch_random_sweep():
     assert np.array_equal(oracle.e4m3_encode(v), ref)
 
 
+def test_e4m3_encode_every_fp32_in_range_matches_torch():
+    # every positive fp32 bit pattern from 2^-12 (below half the smallest
+    # subnormal, 2^-9, everything rounds to zero) up to 464 (above it torch's
+    # conversion gives NaN where the oracle saturates), 22 binades, one at a
+    # time; negative values on every 7th pattern
+    sig = np.arange(1 << 23, dtype=np.uint32)
+    for e in range(127 - 12, 127 + 9):
+        pos = ((np.uint32(e) << 23) | sig).view(np.float32)
+        pos = pos[pos < 464.0]
+        for v in (pos, -pos[::7]):
+            ref = torch.from_numpy(v).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+            got = oracle.e4m3_encode(v)
+            assert np.array_equal(got, ref), (e, int(np.flatnonzero(got != ref)[0]))
+
+
 def test_e4m3_saturation_nan_and_signed_zero():
     v = np.array([448.0, next_up(448.0), 464.0, 480.0, 1e30, np.inf, -np.inf, -500.0,
                   np.nan, -0.0, 0.0, -1e-30, 2.0 ** -10, -(2.0 ** -10),
@@ -124,6 +141,29 @@ E2M1_CASES = [
 def test_e2m1_boundaries(v, code):
     assert oracle.e2m1_encode(np.array([v], np.float32))[0] == code
     assert oracle.e2m1_encode(np.array([-v], np.float32))[0] == (0x8 | code)
+
+
+def e2m1_rne_by_midpoints(v):
+    """Round-to-nearest-even E2M1 magnitude code of |v|, from the definition:
+    the number of midpoints of the value set below |v|, with a value on a
+    midpoint going to the neighbour whose mantissa bit (the code's low bit)
+    is 0; above 6 the largest code (saturation)."""
+    mids = np.array([0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5.0], np.float32)
+    a = np.abs(v)
+    idx = np.searchsorted(mids, a, side="left")            # midpoints strictly below
+    on_mid = (idx < 7) & (a == mids[np.minimum(idx, 6)])
+    return np.where(on_mid & (idx % 2 == 1), idx + 1, idx).astype(np.uint8)
+
+
+def test_e2m1_encode_every_fp32_in_range_matches_rne_definition():
+    # every fp32 bit pattern in [2^-4, 16), both signs: below 2^-4 all round
+    # to zero and above 6 all saturate (both checked by the boundary cases)
+    sig = np.arange(1 << 23, dtype=np.uint32)
+    for e in range(127 - 4, 127 + 4):
+        pos = ((np.uint32(e) << 23) | sig).view(np.float32)
+        want = e2m1_rne_by_midpoints(pos)
+        assert np.array_equal(oracle.e2m1_encode(pos), want), e
+        assert np.array_equal(oracle.e2m1_encode(-pos), want | np.uint8(8)), e
 
 
 def test_e2m1_nearest_on_random_values():
