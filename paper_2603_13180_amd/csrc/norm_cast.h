@@ -122,10 +122,8 @@ typedef short short2_t __attribute__((ext_vector_type(2)));
 // Before use it was checked on the device, on all 2^32 fp32 inputs and for
 // scale exponents -127, -7, 5 and 120, against an integer-rounding E4M3
 // encoder (fp32 significand rounded to 3 bits, ties to even, exponent
-// rebiased; n * 2^-9 with n = rint(|v| * 512) below 2^-6);
-// tests/test_gpu_hw_convert.py repeats that over every input of the range
-// that decides a code, and the GPU parity tests hold the kernels to the
-// oracle.
+// rebiased; n * 2^-9 with n = rint(|v| * 512) below 2^-6); the GPU parity
+// tests hold it to the oracle.
 __device__ __forceinline__ uint32_t e4m3x4_hw(float t0, float t1, float t2, float t3,
                                               float scale)
 {
