@@ -403,13 +403,15 @@ enum Kind : int { K_RMS = 0, K_MXN = 1, K_CAST = 2, K_MXN_POST = 3 };
 
 // Waves per SIMD the register allocation must allow.  A kernel that keeps
 // the row in registers and waits for it once per row hides that wait with
-// other waves: 8 per SIMD (64 VGPRs) fit the E8M0 kernels without spilling;
-// the gain, NVFP4 and multi-wave-team kernels need more registers and take
-// what they get.
+// other waves: 7 per SIMD (72 VGPRs) hold the E8M0 kernels with the row's
+// block maxima kept from the statistics pass (at 8 per SIMD those spill; at
+// 8 without them, recomputing the maxima in the cast pass, the kernel was 1%
+// slower on MI355X); the gain, NVFP4 and multi-wave-team kernels need more
+// registers and take what they get.
 template <int TL, int F, bool GAM>
 constexpr int min_waves()
 {
-    return (GAM || Fmt<F>::NV || TL > 64) ? 1 : 8;
+    return (GAM || Fmt<F>::NV || TL > 64) ? 1 : 7;
 }
 
 // F: output format.  KIND: see Kind.  GAM: apply gamma (RMSNorm and cast).  Workgroup b handles rows b*TEAMS .. b*TEAMS+TEAMS-1, one per team.
@@ -487,12 +489,14 @@ norm_cast_kernel(Args A)
 
         // ---- pass 1: the row statistic ----
         double s = 0.0;
+        uint32_t mb[MXN ? CPL : 1]; // the blocks' absmax patterns, for pass 2
         if constexpr (MXN) {
 #pragma unroll
             for (int j = 0; j < CPL; ++j) {
                 if (j >= cpl)
                     break;
                 const uint32_t m = block_max<BL>(chunk_absmax_bits(v[j]));
+                mb[j] = m;
                 // every lane of the block adds its term: the sum is BL times
                 // the block sum, removed exactly (BL is a power of two) below
                 if constexpr (POST) {
@@ -563,11 +567,9 @@ norm_cast_kernel(Args A)
             // block maximum of |t|
             float a;
             if constexpr (MXN) {
-                // = max |t| (RN is monotone).  The block maximum is taken
-                // again from the raw row rather than kept from pass 1: the
-                // few max and DPP operations cost less than the registers,
-                // which keep the kernel at 8 waves per SIMD
-                a = __uint_as_float(block_max<BL>(chunk_absmax_bits(v[j])) << 16) * rho;
+                // = max |t| (RN is monotone), from the block maximum kept
+                // from pass 1
+                a = __uint_as_float(mb[j] << 16) * rho;
             } else {
                 // integer max of the magnitude patterns: NaN propagates
                 uint32_t m = 0;
