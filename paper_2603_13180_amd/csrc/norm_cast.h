@@ -702,12 +702,65 @@ norm_cast_kernel(Args A)
     }
 }
 
+// Workgroups per compute unit the gain-free kernels with one-wave teams run
+// best at (each such workgroup puts one wave on each SIMD), per output
+// format and kernel; 0 = as many as the registers allow.  Measured on
+// MI355X at [32768, 4096]: the 4-bit formats write in small pieces and lose
+// 2-5% when more rows are in flight (MXNorm E2M1 57.4 us at 8 per CU, 54.4
+// at 4; MXNorm NVFP4 57.9 at 8, 56.6 at 5); E4M3 gains a little at 6 (MXNorm
+// 64.3 -> 64.1 us, RMSNorm 65.1 -> 64.3).  RMSNorm NVFP4 runs best at the 7
+// its registers allow (59.5 us; 60.1 at 5).  The gain kernels already run
+// at 5 (their register count) and are left alone.
+template <int F, int KIND>
+constexpr int wg_per_cu()
+{
+    return Fmt<F>::NV ? (KIND == K_RMS ? 0 : 5) : Fmt<F>::FP4 ? 4 : 6;
+}
+
+// LDS bytes per compute unit of the current device (160 KiB on gfx950), or
+// 0 if the runtime does not say
+inline size_t lds_per_cu()
+{
+    int dev = 0, v = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) !=
+            hipSuccess || v <= 0)
+        return 0;
+    return (size_t)v;
+}
+
+// Dynamic LDS that caps the kernel at wg_per_cu<F, KIND>() workgroups per compute
+// unit: the workgroup's total LDS is set between a (cap+1)-th and a cap-th of
+// the unit's.  The memory is never touched; it only limits occupancy.
+template <int TL, int CPL, int F, int KIND, bool GAM>
+size_t occupancy_lds()
+{
+    if constexpr (GAM || TL > 64 || wg_per_cu<F, KIND>() == 0) {
+        return 0;
+    } else {
+        static const size_t dyn = []() -> size_t {
+            const size_t per_cu = lds_per_cu();
+            hipFuncAttributes fa;
+            if (per_cu == 0 ||
+                hipFuncGetAttributes(&fa, reinterpret_cast<const void *>(
+                                              &norm_cast_kernel<TL, CPL, F, KIND, GAM>)) != hipSuccess)
+                return 0;
+            const size_t cap = (size_t)wg_per_cu<F, KIND>();
+            const size_t lo = per_cu / (cap + 1) + 1024, hi = per_cu / cap;
+            const size_t total = (lo + hi) / 2 / 512 * 512;
+            return total > fa.sharedSizeBytes && total <= 65536 ? total - fa.sharedSizeBytes : 0;
+        }();
+        return dyn;
+    }
+}
+
 template <int TL, int CPL, int F, int KIND, bool GAM>
 hipError_t launch_one(const Args &A, hipStream_t stream)
 {
     const int64_t blocks = (A.T + Team<TL>::TEAMS - 1) / Team<TL>::TEAMS;
+    const size_t dyn_lds = occupancy_lds<TL, CPL, F, KIND, GAM>();
     hipLaunchKernelGGL((norm_cast_kernel<TL, CPL, F, KIND, GAM>), dim3((unsigned)blocks),
-                       dim3(Team<TL>::BLOCK), 0, stream, A);
+                       dim3(Team<TL>::BLOCK), dyn_lds, stream, A);
     return hipGetLastError();
 }
 
