@@ -217,11 +217,11 @@ def test_mx_cast_t_rejects_bad_arguments(args, status):
 
 def test_ste_workspace_size():
     # one float partial row of grad_gamma per workgroup of rpw rows, rpw =
-    # clamp(ceil(T / 512), 4, 32), then 16 double rows of the reduction's slices
+    # clamp(ceil(T / 512), 4, 64), then 16 double rows of the reduction's slices
     lib = mxnorm.load()
     assert lib.mxnorm_ste_bwd_workspace_bytes(0, 4096) == 0
     for T in (1, 4, 5, 32, 33, 2048, 4096, 4097, 32768, 100000):
-        rpw = max(4, min(32, -(-T // 512)))
+        rpw = max(4, min(64, -(-T // 512)))
         assert lib.mxnorm_ste_bwd_workspace_bytes(T, 4096) == \
             -(-T // rpw) * 4096 * 4 + 16 * 4096 * 8, T
 
