@@ -199,8 +199,8 @@ typedef enum {
  * code gives NaN; results beyond the float range are infinite.
  * block: 32 (other sizes: MX_EUNSUPPORTED).  elem: mx_elem.  Requirements:
  * K a multiple of 128 (E4M3) or 256 (E2M1) and at most MX_MATMUL_MAX_K, N a
- * multiple of 16 (else MX_EUNSUPPORTED); codes 16-byte, scales 4-byte, out 16-byte (f32) or
- * 8-byte (bf16) aligned.  M == 0 or N == 0 is a no-op.  Asynchronous on
+ * multiple of 16 (else MX_EUNSUPPORTED); codes 16-byte, scales 4-byte and out
+ * 16-byte aligned (else MX_EINVAL).  M == 0 or N == 0 is a no-op.  Asynchronous on
  * `stream`; nothing is allocated.
  */
 mx_status mx_matmul_fwd(const uint8_t *a_codes, const uint8_t *a_scales, const uint8_t *b_codes,

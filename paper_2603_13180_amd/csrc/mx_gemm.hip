@@ -358,33 +358,61 @@ __global__ void __launch_bounds__(NT) mx_gemm_kernel(Args A)
     }
 
     // lane (g, qd) of tile (i, j) holds H[m][n .. n+3] with
-    // m = m0 + wm + 16 j + qd and n = n0 + wn + 16 i + 4 g
-#pragma unroll
-    for (int j = 0; j < FM; ++j) {
-        const int64_t m = m0 + wm + 16 * j + qd;
-        if (m >= A.M)
-            continue;
-#pragma unroll
-        for (int i = 0; i < FN; ++i) {
+    // m = m0 + wm + 16 j + qd and n = n0 + wn + 16 i + 4 g.  N is a multiple
+    // of 16, so a tile column base below N has its 16 columns inside H.
+    auto gained = [&](int i, int j) {
+        v4f v = acc[i][j];
+        if (A.bgain) {
             const int64_t n = n0 + wn + 16 * i + 4 * g;
-            if (n >= A.N)
-                continue;
-            v4f v = acc[i][j];
-            if (A.bgain) {
-                const uint2 gw = *reinterpret_cast<const uint2 *>(A.bgain + n);
-                v[0] = v[0] * __uint_as_float(gw.x << 16);
-                v[1] = v[1] * __uint_as_float(gw.x & 0xFFFF0000u);
-                v[2] = v[2] * __uint_as_float(gw.y << 16);
-                v[3] = v[3] * __uint_as_float(gw.y & 0xFFFF0000u);
+            const uint2 gw = *reinterpret_cast<const uint2 *>(A.bgain + (n < A.N ? n : 0));
+            v[0] = v[0] * __uint_as_float(gw.x << 16);
+            v[1] = v[1] * __uint_as_float(gw.x & 0xFFFF0000u);
+            v[2] = v[2] * __uint_as_float(gw.y << 16);
+            v[3] = v[3] * __uint_as_float(gw.y & 0xFFFF0000u);
+        }
+        return v;
+    };
+    if constexpr (OUT == MX_OUT_F32) {
+#pragma unroll
+        for (int j = 0; j < FM; ++j) {
+            const int64_t m = m0 + wm + 16 * j + qd;
+#pragma unroll
+            for (int i = 0; i < FN; ++i) {
+                const int64_t n = n0 + wn + 16 * i + 4 * g;
+                const v4f v = gained(i, j);
+                if (m < A.M && n < A.N)
+                    *reinterpret_cast<float4 *>(static_cast<float *>(A.out) + m * A.N + n) =
+                        make_float4(v[0], v[1], v[2], v[3]);
             }
-            if constexpr (OUT == MX_OUT_F32) {
-                *reinterpret_cast<float4 *>(static_cast<float *>(A.out) + m * A.N + n) =
-                    make_float4(v[0], v[1], v[2], v[3]);
-            } else {
-                const uint32_t lo = f32_to_bf16_rne(v[0]) | ((uint32_t)f32_to_bf16_rne(v[1]) << 16);
-                const uint32_t hi = f32_to_bf16_rne(v[2]) | ((uint32_t)f32_to_bf16_rne(v[3]) << 16);
-                *reinterpret_cast<uint2 *>(static_cast<uint16_t *>(A.out) + m * A.N + n) =
-                    make_uint2(lo, hi);
+        }
+    } else {
+        // bf16: tiles i and i+1 are stored together.  v_permlane16_swap
+        // trades the odd lane rows (g = 1, 3) of tile i's values with the
+        // even lane rows (g = 0, 2) of tile i+1's, after which lane row g
+        // holds 8 adjacent columns, 16 bytes, of tile i + (g & 1) from
+        // column 8 (g >> 1): one 16-byte store per lane and tile pair
+        // instead of two 8-byte stores.  The swap runs on every lane; only
+        // the stores are masked.
+        static_assert(FN % 2 == 0, "tiles are stored in pairs");
+        typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
+#pragma unroll
+        for (int j = 0; j < FM; ++j) {
+            const int64_t m = m0 + wm + 16 * j + qd;
+#pragma unroll
+            for (int i = 0; i < FN; i += 2) {
+                uint32_t lo[2], hi[2];
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const v4f v = gained(i + h, j);
+                    lo[h] = f32_to_bf16_rne(v[0]) | ((uint32_t)f32_to_bf16_rne(v[1]) << 16);
+                    hi[h] = f32_to_bf16_rne(v[2]) | ((uint32_t)f32_to_bf16_rne(v[3]) << 16);
+                }
+                const auto sl = __builtin_amdgcn_permlane16_swap(lo[0], lo[1], false, false);
+                const auto sh = __builtin_amdgcn_permlane16_swap(hi[0], hi[1], false, false);
+                const int64_t n = n0 + wn + 16 * (i + (g & 1)) + 8 * (g >> 1);
+                if (m < A.M && n < A.N)
+                    *reinterpret_cast<u32x4v *>(static_cast<uint16_t *>(A.out) + m * A.N + n) =
+                        u32x4v{sl[0], sh[0], sl[1], sh[1]};
             }
         }
     }
@@ -435,10 +463,10 @@ mx_status mx_matmul_fwd(const uint8_t *a_codes, const uint8_t *a_scales, const u
     if (!a_codes || !a_scales || !b_codes || !b_scales || !out)
         return mxk::fail(MX_EINVAL, "NULL pointer");
     if (!aligned(a_codes, 16) || !aligned(b_codes, 16) || !aligned(a_scales, 4) ||
-        !aligned(b_scales, 4) || !aligned(out, out_dtype == MX_OUT_F32 ? 16 : 8) ||
+        !aligned(b_scales, 4) || !aligned(out, 16) ||
         (b_gain && !aligned(b_gain, 8)))
-        return mxk::fail(MX_EINVAL, "codes must be 16-byte, scales 4-byte, out 16-byte (f32) or "
-                               "8-byte (bf16) and b_gain 8-byte aligned");
+        return mxk::fail(MX_EINVAL, "codes and out must be 16-byte, scales 4-byte and b_gain "
+                               "8-byte aligned");
     const int64_t tm = (M + mxg::BM - 1) / mxg::BM, tn = (N + mxg::BN - 1) / mxg::BN;
     if (tm * tn > INT32_MAX / 2 || M > INT32_MAX || N > INT32_MAX)
         return mxk::fail(MX_EUNSUPPORTED, "problem too large");

@@ -188,6 +188,7 @@ def test_mx_cast_rejects_bad_arguments():
     (dict(N=24), 2), (dict(a=None), 1), (dict(out=None), 1), (dict(a=A8), 1),
     (dict(bs=OUT + 2), 1), (dict(out=A8), 1), (dict(M=0, a=None, out=None), 0),
     (dict(N=0, b=None, out=None), 0), (dict(gain=OUT + 4), 1), (dict(K=1 << 23), 2),
+    (dict(out=A8, out_dtype=1), 1),    # bf16 output is stored 16 bytes at a time
 ])
 def test_mx_matmul_rejects_bad_arguments(args, status):
     lib = mxnorm.load()
