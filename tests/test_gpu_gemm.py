@@ -99,10 +99,15 @@ def one_hot_operand(rows, K, elem, pos, rng):
     return c, s
 
 
+@pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
 @pytest.mark.parametrize("elem", ELEMS)
-def test_single_products_are_exact(elem):
+def test_single_products_are_exact(elem, out_dtype):
     # every k of a 512-wide K appears; each output is 0 or one product, which
-    # fp32 holds exactly -- a wrong k pairing or scale association shows
+    # fp32 holds exactly -- a wrong k pairing or scale association shows.  In
+    # bf16 each output is that product rounded once to nearest even (torch's
+    # CPU conversion), so a column written to the wrong place shows as well
+    # (N = 528 leaves the last 256-column tile with one 16-column tile of
+    # values beside one past N)
     K = 512
     M, N = 640, 528
     rng = np.random.default_rng(5)
@@ -110,9 +115,13 @@ def test_single_products_are_exact(elem):
     pb = (np.arange(N) * 7) % K
     ac, as_ = one_hot_operand(M, K, elem, pa, rng)
     bc, bs = one_hot_operand(N, K, elem, pb, rng)
-    got = gpu_matmul(ac, as_, bc, bs, K, elem)
+    got = gpu_matmul(ac, as_, bc, bs, K, elem, out_dtype)
     want = oracle.mx_matmul(ac, as_, bc, bs, K, elem=elem)
     assert (want != 0).sum() >= M // 8
+    if out_dtype == torch.bfloat16:
+        want32 = want.astype(np.float32)
+        assert np.array_equal(want32.astype(np.float64), want)   # one product: exact in fp32
+        want = torch.from_numpy(want32).to(torch.bfloat16).float().numpy().astype(np.float64)
     bad = np.argwhere(got != want)
     assert bad.size == 0, "%d outputs differ, first %s: got %r want %r" % (
         len(bad), bad[0], got[tuple(bad[0])], want[tuple(bad[0])])
