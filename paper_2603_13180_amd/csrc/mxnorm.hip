@@ -180,35 +180,82 @@ mx_status run(Args A, int fmt, int kind, void *stream)
 // ----------------------------------------------------- post-round table --
 //
 // Post-round MXNorm estimates the RMS as f^-1(Xbar), Xbar the mean of the
-// block absmaxes rounded down to powers of two and f(sigma) = E[max_i
-// r(|X_i|)] for B independent N(0, sigma^2) values (the post-round
-// appendix):  f(sigma) = sum_j 2^j (P(|X| < 2^(j+1))^B - P(|X| < 2^j)^B),
-// P(|X| < x) = erf(x / (sigma sqrt 2)).  Because f(2 sigma) = 2 f(sigma) the
-// inverse is tabulated on [1, 2] at x_i = 2^(i/64) (values rounded to
-// float) and scaled by powers of two in the kernel.
+// block absmaxes rounded down to powers of two and f(sigma) = E[r(M)], with
+// M the largest of B independent |N(0, sigma^2)| values and r(m) =
+// 2^floor(log2 m) (the post-round appendix).  Because f(2 sigma) = 2
+// f(sigma) the inverse is tabulated on [1, 2] at x_i = 2^(i/64) (values
+// rounded to float) and scaled by powers of two in the kernel.
+//
+// The library evaluates f through the layer-cake identity rather than the
+// appendix's sum over the events {r(M) = 2^j}: r(m) = sum over j with
+// 2^j <= m of 2^(j-1), so
+//     f(sigma) = sum_j 2^(j-1) P(M >= 2^j) = sum_j 2^(j-1) (1 - F_j^B),
+// F_j = erf(2^j / (sigma sqrt 2)).  1 - F^B is formed from erfc so that the
+// upper terms keep their relative precision.  For the sigmas the table
+// needs (about 0.3 .. 3) every term below j = kLow has F_j^B < 2^-600, so it
+// equals 2^(j-1) in double and their sum is the closed form 2^(kLow-1);
+// above j = kHigh the terms are zero.  The root of f(sigma) = x is then found by
+// Newton's method on the analytic derivative
+//     f'(sigma) = sum_j 2^(j-1) B F_j^(B-1) (2/sqrt(pi)) e^(-u_j^2) u_j / sigma,
+// u_j = 2^j / (sigma sqrt 2), kept inside a bracket that halving the step
+// falls back to.
 
-double series_f(double sigma, int B)
+constexpr int kLow = -40, kHigh = 40;
+
+// P(M >= 2^j) = 1 - erf(u)^B, u = 2^j / (sigma sqrt 2)
+double tail_prob(double u, int B)
 {
-    double acc = 0.0;
-    for (int j = -64; j <= 64; ++j) {
-        const double a = std::pow(std::erf(std::ldexp(1.0, j + 1) / sigma / std::sqrt(2.0)), B);
-        const double b = std::pow(std::erf(std::ldexp(1.0, j) / sigma / std::sqrt(2.0)), B);
-        acc += std::ldexp(1.0, j) * (a - b);
-    }
-    return acc;
+    const double q = std::erfc(u);
+    if (q < 0.5)
+        return -std::expm1((double)B * std::log1p(-q));
+    return 1.0 - std::pow(std::erf(u), (double)B);
 }
 
-// f is increasing: halve a bracket around x until it stops shrinking
-double series_f_inverse(double x, int B)
+// f(sigma) and f'(sigma) together
+void layer_cake_f(double sigma, int B, double &f, double &df)
 {
-    double lo = x / 16.0, hi = x * 16.0;
-    for (int it = 0; it < 200; ++it) {
-        const double mid = 0.5 * (lo + hi);
-        if (mid == lo || mid == hi)
-            break;
-        (series_f(mid, B) < x ? lo : hi) = mid;
+    const double inv_s2 = 1.0 / (sigma * std::sqrt(2.0));
+    const double c = 2.0 / std::sqrt(M_PI);
+    f = std::ldexp(1.0, kLow - 1); // the terms j < kLow, each 2^(j-1) exactly
+    df = 0.0;
+    for (int j = kLow; j <= kHigh; ++j) {
+        const double w = std::ldexp(1.0, j - 1);
+        const double u = std::ldexp(inv_s2, j);
+        f += w * tail_prob(u, B);
+        const double g = std::erf(u);
+        if (g > 0.0)
+            df += w * (double)B * std::pow(g, (double)(B - 1)) * c * std::exp(-u * u) * u / sigma;
     }
-    return 0.5 * (lo + hi);
+}
+
+// f^-1(x) for x > 0: bracket by powers of two (f(2 s) = 2 f(s)), then
+// Newton steps, replaced by the bracket's midpoint whenever a step would
+// leave the bracket; stop when a step no longer changes sigma by more than
+// a few units in the last place.
+double layer_cake_inverse(double x, int B)
+{
+    double f, df;
+    double lo = x, hi = x;
+    for (layer_cake_f(lo, B, f, df); f > x; layer_cake_f(lo, B, f, df))
+        lo *= 0.5;
+    for (layer_cake_f(hi, B, f, df); f < x; layer_cake_f(hi, B, f, df))
+        hi *= 2.0;
+    double s = 0.5 * (lo + hi);
+    for (int it = 0; it < 100; ++it) {
+        layer_cake_f(s, B, f, df);
+        const double r = f - x;
+        if (r == 0.0)
+            return s;
+        (r < 0.0 ? lo : hi) = s;
+        double next = df > 0.0 ? s - r / df : 0.5 * (lo + hi);
+        if (!(next > lo && next < hi))
+            next = 0.5 * (lo + hi);
+        const bool done = std::fabs(next - s) <= 4.0 * DBL_EPSILON * s;
+        s = next;
+        if (done)
+            break;
+    }
+    return s;
 }
 
 struct PostTable {
@@ -223,8 +270,8 @@ const PostTable &post_table(int B)
     const int k = B == 16 ? 0 : B == 32 ? 1 : 2;
     std::call_once(once[k], [&] {
         for (int i = 0; i <= 64; ++i) {
-            tab[k].x[i] = (float)std::exp2((double)i / 64.0);
-            tab[k].v[i] = (float)series_f_inverse((double)tab[k].x[i], B);
+            tab[k].x[i] = (float)std::pow(2.0, (double)i / 64.0);
+            tab[k].v[i] = (float)layer_cake_inverse((double)tab[k].x[i], B);
         }
     });
     return tab[k];

@@ -29,7 +29,7 @@ LIB = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhwconvert.so"
 @pytest.fixture(scope="module")
 def hwc():
     if not torch.cuda.is_available():
-        pytest.skip("no GPU")
+        raise RuntimeError("the conversion-instruction test needs a GPU (run it with -m gpu)")
     if not os.path.exists(LIB):
         pytest.fail("tests/libhwconvert.so is missing: run __graft_entry__.build()")
     lib = ctypes.CDLL(LIB)
