@@ -252,6 +252,28 @@ mx_status mxnorm_ste_bwd(const void *x, const void *grad_z, const void *gamma, c
                          void *workspace, size_t workspace_bytes, void *stream);
 
 /*
+ * mxnorm_ste_bwd without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  Same arguments, arithmetic, outputs and
+ * errors as mxnorm_ste_bwd; the grad_gamma partial rows and slices go to a
+ * static device array of mxnorm_ste_bwd_noalloc_max_workspace() bytes
+ * (32 MiB) that each GPU holds for the life of the process.  It calls no
+ * hipMalloc, hipFree or allocating library routine.  Returns MX_EUNSUPPORTED,
+ * before any launch, when grad_gamma is requested and
+ * mxnorm_ste_bwd_workspace_bytes(T, d) exceeds that size (for example
+ * T = 32768 fits up to d = 14336).  The device is the stream's (the current
+ * device for the null stream); its array's address is looked up on the first
+ * call on that device.  All calls on one GPU share its array: calls that
+ * overlap in time on one GPU (on different streams, or from several host
+ * threads) race and give wrong grad_gamma.  Every byte a call reads from the
+ * array is written earlier in the same call, so nothing needs clearing.
+ */
+size_t mxnorm_ste_bwd_noalloc_max_workspace(void);
+mx_status mxnorm_ste_bwd_noalloc(const void *x, const void *grad_z, const void *gamma,
+                                 const float *rho, int64_t T, int64_t d, int out_dtype,
+                                 void *grad_x, float *grad_gamma, void *stream);
+
+/*
  * Default NVFP4 tensor decode scales: an output bound divided by 6 * 448, so
  * the bound maps to the largest E2M1 x E4M3 magnitude.  MXNorm: Lemma 2's
  * bound K^(1/p) / coef (K = d / block; coef <= 0 selects the table value);

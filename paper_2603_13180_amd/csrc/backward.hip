@@ -19,6 +19,8 @@
 // 3.3x slower with the hint; the STE 6% slower).
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 #include <stdint.h>
 
 #include <algorithm>
@@ -614,6 +616,57 @@ bool aligned(const void *p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0;
 
 int64_t ste_workgroups(int64_t T) { return (T + mxb::ste_rpw(T) - 1) / mxb::ste_rpw(T); }
 
+// Device-resident workspace of mxnorm_ste_bwd_noalloc: the grad_gamma partial
+// rows and slices live here instead of in caller memory.  Each GPU the
+// library runs on holds its own copy for the life of the process.  In host
+// code `scratch` only names the symbol; its device address (one per GPU) is
+// looked up once per device with hipGetSymbolAddress and kept in
+// scratch_ptr.
+constexpr size_t kScratchBytes = size_t(32) << 20;
+constexpr int kMaxDevices = 64;
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+std::mutex scratch_mu;
+void *scratch_ptr[kMaxDevices];
+
+// The scratch address on the device that `stream` belongs to (the current
+// device for the null stream), or an error.
+mx_status scratch_for(void *stream, void **out)
+{
+    int dev = -1;
+    hipError_t e;
+    if (stream) {
+        hipDevice_t hd;
+        e = hipStreamGetDevice(static_cast<hipStream_t>(stream), &hd);
+        dev = (int)hd;
+    } else {
+        e = hipGetDevice(&dev);
+    }
+    if (e != hipSuccess)
+        return mxk::fail(MX_EHIP, "cannot find the stream's device: %s", hipGetErrorString(e));
+    if (dev < 0 || dev >= kMaxDevices)
+        return mxk::fail(MX_EUNSUPPORTED, "device %d is beyond the %d the library tracks", dev,
+                         kMaxDevices);
+    std::lock_guard<std::mutex> lock(scratch_mu);
+    if (!scratch_ptr[dev]) {
+        int cur = -1;
+        if ((e = hipGetDevice(&cur)) != hipSuccess)
+            return mxk::fail(MX_EHIP, "hipGetDevice failed: %s", hipGetErrorString(e));
+        if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess)
+            return mxk::fail(MX_EHIP, "hipSetDevice(%d) failed: %s", dev, hipGetErrorString(e));
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (cur != dev)
+            (void)hipSetDevice(cur);
+        if (e != hipSuccess || !p)
+            return mxk::fail(MX_EHIP, "hipGetSymbolAddress(scratch) failed on device %d: %s", dev,
+                             hipGetErrorString(e));
+        scratch_ptr[dev] = p;
+    }
+    *out = scratch_ptr[dev];
+    return MX_OK;
+}
+
 } // namespace
 
 extern "C" {
@@ -749,6 +802,31 @@ mx_status mxnorm_ste_bwd(const void *x, const void *grad_z, const void *gamma, c
     if (e != hipSuccess)
         return mxk::fail(MX_EHIP, "kernel launch failed: %s", hipGetErrorString(e));
     return MX_OK;
+}
+
+size_t mxnorm_ste_bwd_noalloc_max_workspace(void) { return kScratchBytes; }
+
+mx_status mxnorm_ste_bwd_noalloc(const void *x, const void *grad_z, const void *gamma,
+                                 const float *rho, int64_t T, int64_t d, int out_dtype,
+                                 void *grad_x, float *grad_gamma, void *stream)
+{
+    mxk::clear_error();
+    if (grad_gamma && T > 0 && d > 0 && mxnorm_ste_bwd_workspace_bytes(T, d) > kScratchBytes)
+        return mxk::fail(MX_EUNSUPPORTED,
+                         "grad_gamma at T = %lld, d = %lld needs %zu bytes of workspace, more "
+                         "than the %zu the allocation-free entry point holds",
+                         (long long)T, (long long)d, mxnorm_ste_bwd_workspace_bytes(T, d),
+                         kScratchBytes);
+    void *ws = nullptr;
+    if (grad_gamma && T > 0) {
+        const mx_status st = scratch_for(stream, &ws);
+        if (st != MX_OK)
+            return st;
+    }
+    // every partial row and slice is written before it is read, so the
+    // scratch needs no clearing between calls
+    return mxnorm_ste_bwd(x, grad_z, gamma, rho, T, d, out_dtype, grad_x, grad_gamma, ws,
+                          ws ? kScratchBytes : 0, stream);
 }
 
 } // extern "C"

@@ -58,6 +58,8 @@ def load():
         "mx_cast_t_fwd": (I, [P, P, I64, I64, I, I, I, P, P, P]),
         "mxnorm_ste_bwd_workspace_bytes": (ctypes.c_size_t, [I64, I64]),
         "mxnorm_ste_bwd": (I, [P, P, P, P, I64, I64, I, P, P, P, ctypes.c_size_t, P]),
+        "mxnorm_ste_bwd_noalloc_max_workspace": (ctypes.c_size_t, []),
+        "mxnorm_ste_bwd_noalloc": (I, [P, P, P, P, I64, I64, I, P, P, P]),
         "mxnorm_default_global_scale": (F, [I64, I, I, F]),
         "rmsnorm_default_global_scale": (F, [I64, F]),
         "mxnorm_coef": (F, [I, I]),
@@ -360,6 +362,34 @@ def mxnorm_ste_bwd(x, grad_z, gamma, rho, out_dtype=torch.bfloat16, want_grad_ga
                               _ptr(workspace) if want_grad_gamma else None, ws_bytes,
                               _stream(x.device)))
     return grad_x, (grad_gamma if want_grad_gamma else None)
+
+
+def mxnorm_ste_bwd_noalloc(x, grad_z, gamma, rho, grad_x, grad_gamma=None):
+    """mxnorm_ste_bwd through the library's allocation-free entry point: the
+    grad_gamma workspace is the library's static device array, so neither the
+    library nor this call allocates.  The caller passes the outputs: grad_x
+    [T, d] (float32 or bfloat16, its dtype selects the output type) and
+    grad_gamma float32 [d] or None.  Calls that overlap in time on one GPU
+    share that array and race."""
+    T, d = _input(x)
+    if grad_z.dtype != torch.bfloat16 or grad_z.shape != x.shape or grad_z.device != x.device \
+            or not grad_z.is_contiguous():
+        raise ValueError("grad_z must be a contiguous bfloat16 tensor shaped like x")
+    g = _gamma(gamma, x)
+    if rho.dtype != torch.float32 or rho.shape != (T,) or rho.device != x.device \
+            or not rho.is_contiguous():
+        raise ValueError("rho must be contiguous float32 [T] on x's device")
+    if grad_x.dtype not in OUT_DTYPES or grad_x.shape != x.shape or grad_x.device != x.device \
+            or not grad_x.is_contiguous():
+        raise ValueError("grad_x must be a contiguous float32 or bfloat16 tensor shaped like x")
+    if grad_gamma is not None and (grad_gamma.dtype != torch.float32 or grad_gamma.shape != (d,)
+                                   or grad_gamma.device != x.device):
+        raise ValueError("grad_gamma must be float32 [d] on x's device")
+    _check(load().mxnorm_ste_bwd_noalloc(_ptr(x), _ptr(grad_z), _ptr(g), _ptr(rho), T, d,
+                                         OUT_DTYPES[grad_x.dtype], _ptr(grad_x),
+                                         _ptr(grad_gamma) if grad_gamma is not None else None,
+                                         _stream(x.device)))
+    return grad_x, grad_gamma
 
 
 def mxnorm_linear_bwd(grad_h, x, rho, gamma, w, block=32, elem="e4m3",

@@ -242,6 +242,34 @@ def test_ste_rejects_bad_arguments(args, status):
                               kw["out"], kw["gx"], kw["gg"], kw["ws"], kw["wsb"], None) == status
 
 
+def test_ste_noalloc_rejects_sizes_beyond_its_array():
+    # the allocation-free entry point holds 32 MiB of grad_gamma workspace per
+    # GPU; larger problems are refused on the host, before any HIP call
+    lib = mxnorm.load()
+    cap = lib.mxnorm_ste_bwd_noalloc_max_workspace()
+    assert cap == 32 << 20
+    assert lib.mxnorm_ste_bwd_workspace_bytes(32768, 14336) <= cap
+    for T, d in ((131072, 8192), (32768, 16384), (1 << 20, 4096)):
+        assert lib.mxnorm_ste_bwd_workspace_bytes(T, d) > cap
+        assert lib.mxnorm_ste_bwd_noalloc(A16, A16, None, OUT, T, d, 1, OUT, OUT, None) == 2
+        assert b"allocation-free" in lib.mx_last_error()
+
+
+@pytest.mark.parametrize("args,status", [
+    (dict(T=-1), 1), (dict(d=12), 1), (dict(d=65536), 2), (dict(out=2), 1), (dict(x=None), 1),
+    (dict(rho=None), 1), (dict(gx=None), 1), (dict(x=A8), 1),
+    (dict(T=0, x=None, gz=None, rho=None, gx=None), 0),
+])
+def test_ste_noalloc_rejects_bad_arguments(args, status):
+    # without grad_gamma the scratch array is not touched, so every check
+    # runs on the host
+    lib = mxnorm.load()
+    kw = dict(x=A16, gz=A16, gamma=None, rho=OUT, T=4, d=64, out=1, gx=OUT)
+    kw.update(args)
+    assert lib.mxnorm_ste_bwd_noalloc(kw["x"], kw["gz"], kw["gamma"], kw["rho"], kw["T"], kw["d"],
+                                      kw["out"], kw["gx"], None, None) == status
+
+
 @pytest.mark.parametrize("block", [16, 32, 64])
 def test_postround_table_equals_oracle_table(block):
     # computed independently on both sides from the appendix's series; the
