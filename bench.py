@@ -429,26 +429,93 @@ def time_launches(fn, n_sets, steps, warmup, stream):
     return start.elapsed_time(end) / steps  # ms per launch
 
 
-def cpu_baseline(x_rows, d, budget_s=10.0):
-    """The oracle as it stands, single-threaded, on the first rows of the same
-    workload until about budget_s of CPU time has been spent."""
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+# every workload preset, with the oracle entry point that computes it
+CPU_CONFIGS = (("llama3-125m-d768", "mxfp8"), ("llama3-1b-d2048", "mxfp8"),
+               ("llama3-8b-d4096", "mxfp8"), ("llama3-8b-d4096-nvfp4", "nvfp4"),
+               ("llama3-8b-longctx-stress", "mxfp8"))
+
+
+def _oracle_fn(fmt, d):
+    import numpy as np
     import oracle
-    oracle.mxnorm_mxfp8(x_rows[:4])   # builds/loads the library outside the timing
+    if fmt == "mxfp8":
+        return oracle.mxnorm_mxfp8, mxfp8_bytes
+    s_g = float(np.float32(oracle.mxnorm_default_global_scale(d, 16, 2)))
+    return (lambda x: oracle.mxnorm_nvfp4(x, s_g)), nvfp4_bytes
+
+
+def _time_rows(fn, x, budget_s, step=512):
+    """Single-threaded: chunks of `step` rows from the start of x until
+    budget_s has passed or x is used up.  Returns (rows, seconds)."""
+    fn(x[:4])   # builds/loads the library outside the timing
     done = 0
     t0 = time.perf_counter()
-    step = 512
-    while done < x_rows.shape[0] and time.perf_counter() - t0 < budget_s:
-        oracle.mxnorm_mxfp8(x_rows[done:done + step])
+    while done < x.shape[0] and time.perf_counter() - t0 < budget_s:
+        fn(x[done:done + step])
         done += step
-    el = time.perf_counter() - t0
+    return min(done, x.shape[0]), time.perf_counter() - t0
+
+
+def cpu_baseline(x_rows, d, budget_s=10.0, per_config_s=2.0, parallel_rows=32768):
+    """The oracle as it stands on the host cores.  Primary: single-threaded,
+    on the first rows of the headline workload until about budget_s has been
+    spent.  Also: a bounded single-threaded sample of each workload preset,
+    and the same oracle run row-parallel on threads over the cores this
+    process may use (its C calls release the GIL), as a secondary number."""
+    from concurrent.futures import ThreadPoolExecutor
+    import numpy as np
+    from paper_2603_13180_amd import synth
+
+    fn, nbytes = _oracle_fn("mxfp8", d)
+    done, el = _time_rows(fn, x_rows, budget_s)
+    per = {}
+    for name, fmt in CPU_CONFIGS:
+        P = synth.PRESETS[name]
+        rows = min(P.T, 8192)
+        xs = x_rows if name == WORKLOAD else synth.generate(name, rows=np.arange(rows)).x
+        f, nb = _oracle_fn(fmt, P.d)
+        n, t = _time_rows(f, xs[:rows], per_config_s, step=256)
+        per[name] = {"format": fmt, "rows": n, "s": round(t, 2),
+                     "GB/s": round(nb(n, P.d) / t / 1e9, 4), "rows_per_s": round(n / t, 1),
+                     "full_tensor_s_est": round(P.T * t / n, 1)}
+    try:
+        avail = len(os.sched_getaffinity(0))
+    except AttributeError:
+        avail = os.cpu_count() or 1
+    threads = max(1, min(avail, 64))
+    xp = x_rows[:parallel_rows]
+    chunks = [c for c in np.array_split(np.arange(xp.shape[0]), 8 * threads) if len(c)]
+    t0 = time.perf_counter()
+    with ThreadPoolExecutor(threads) as ex:
+        list(ex.map(lambda ix: fn(xp[ix[0]:ix[-1] + 1]), chunks))
+    tp = time.perf_counter() - t0
     return {
-        "value": round(mxfp8_bytes(done, d) / el / 1e9, 4),
+        "value": round(nbytes(done, d) / el / 1e9, 4),
         "unit": "GB/s",
         "cores": 1,
         "kind": "oracle",
         "sample": "first %d rows of %s (%d elements), single-threaded C oracle, %.1f s"
                   % (done, WORKLOAD, done * d, el),
         "rows_per_s": round(done / el, 1),
+        "nproc": os.cpu_count(),
+        "cores_available": avail,
+        "cpu_model": cpu_model(),
+        "per_config": per,
+        "row_parallel": {"threads": threads, "rows": int(xp.shape[0]), "s": round(tp, 2),
+                         "GB/s": round(nbytes(xp.shape[0], d) / tp / 1e9, 4),
+                         "rows_per_s": round(xp.shape[0] / tp, 1),
+                         "sample": "first %d rows of %s, row chunks on %d threads"
+                                   % (xp.shape[0], WORKLOAD, threads)},
     }
 
 
@@ -550,10 +617,15 @@ def main():
     small = [torch.empty(T, d // 32, dtype=torch.uint8, device=dev) for _ in range(n_sets)]
     ref = {}
     for mode, nbytes in (("mixed", b8 - 4 * T), ("read", T * d * 2 + 16 * T),
-                         ("write", T * d + T * (d // 32))):
-        m = time_launches(lambda i: streamref.stream_reference(
-            xs[i], codes[i], small[i] if mode != "read" else small[i][:, :16], mode),
-            n_sets, 50, 5, stream)
+                         ("write", T * d + T * (d // 32)),
+                         ("nvfp4", nvfp4_bytes(T, d) - 4 * T)):
+        def run_ref(i, mode=mode):
+            if mode == "nvfp4":
+                streamref.stream_reference(xs[i], ncodes[i], nscales[i], mode)
+            else:
+                streamref.stream_reference(
+                    xs[i], codes[i], small[i] if mode != "read" else small[i][:, :16], mode)
+        m = time_launches(run_ref, n_sets, 50, 5, stream)
         ref[mode] = round(nbytes / (m * 1e-3) / 1e9, 1)
     dst = torch.empty_like(x0)
     m = time_launches(lambda i: dst.copy_(xs[i]), n_sets, 50, 5, stream)
@@ -624,6 +696,8 @@ def main():
             "speedup_vs_rmsnorm_cast": round(side["rmsnorm_nvfp4"]["ms"] / side["mxnorm_nvfp4"]["ms"], 4),
             "speedup_vs_rmsnorm_gamma_cast":
                 round(side["rmsnorm_nvfp4_gamma"]["ms"] / side["mxnorm_nvfp4"]["ms"], 4),
+            "stream_reference_GBps": ref["nvfp4"],
+            "frac_of_stream_reference": round(side["mxnorm_nvfp4"]["GB/s"] / ref["nvfp4"], 4),
         },
         "kernels": side,
         "mx_matmul": {

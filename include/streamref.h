@@ -13,7 +13,10 @@
  * mode: MX_STREAM_MIXED reads x and writes out [T, d] and out_small
  *       [T, d/32]; MX_STREAM_READ reads x and writes one 16-byte word per
  *       row to out_small (which must hold 16*T bytes); MX_STREAM_WRITE
- *       writes out and out_small without reading x.
+ *       writes out and out_small without reading x; MX_STREAM_NVFP4 has
+ *       the traffic and access pattern of mxnorm_nvfp4_fwd: it reads x,
+ *       writes 4 bytes per 8 elements to out [T, d/2] and one byte per 16
+ *       elements to out_small [T, d/16] (staged in LDS, 16-byte stores).
  * d must be a positive multiple of 512 and at most 4096; x, out and
  * out_small 16-byte aligned device pointers.  Asynchronous on `stream`.
  * Returns 0 on success, 1 for an invalid argument (nothing launched), 3 if
@@ -31,6 +34,7 @@ extern "C" {
 #define MX_STREAM_MIXED 0
 #define MX_STREAM_READ 1
 #define MX_STREAM_WRITE 2
+#define MX_STREAM_NVFP4 3
 
 int mx_stream_reference(const void *x, int64_t T, int64_t d, uint8_t *out, uint8_t *out_small,
                         int mode, void *stream);

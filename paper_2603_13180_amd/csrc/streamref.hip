@@ -21,7 +21,7 @@ template <int MODE>
 __global__ void __launch_bounds__(256) stream_kernel(const uint4 *x, int64_t T, int nc,
                                                      uint8_t *out, uint8_t *out_small)
 {
-    __shared__ __attribute__((aligned(16))) uint8_t sbuf[4 * 128];
+    __shared__ __attribute__((aligned(16))) uint8_t sbuf[4 * 256];
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int64_t row = (int64_t)blockIdx.x * 4 + wave;
@@ -49,7 +49,7 @@ __global__ void __launch_bounds__(256) stream_kernel(const uint4 *x, int64_t T, 
             v[j].w = ok ? v[j].w : 0u;
         }
     }
-    uint8_t *sb = sbuf + wave * 128;
+    uint8_t *sb = sbuf + wave * 256;
     if (MODE == MX_STREAM_READ) {
         uint32_t acc = 0;
 #pragma unroll
@@ -65,18 +65,27 @@ __global__ void __launch_bounds__(256) stream_kernel(const uint4 *x, int64_t T, 
     for (int j = 0; j < 8; ++j) {
         if (row_ok && j < cpl) {
             const int c = j * 64 + lane;
-            const uint2 o = make_uint2((v[j].x >> 8) ^ v[j].y, (v[j].z >> 8) ^ v[j].w);
-            __builtin_nontemporal_store(((unsigned long long)o.y << 32) | o.x,
-                                        reinterpret_cast<unsigned long long *>(
-                                            out + rr * nc * 8 + (int64_t)c * 8));
-            if ((lane & 3) == 0)
-                sb[c >> 2] = (uint8_t)v[j].x;
+            if (MODE == MX_STREAM_NVFP4) {
+                // 4 bytes of codes per 8 elements; one scale byte per 16
+                const uint32_t o = ((v[j].x >> 8) ^ v[j].y) ^ ((v[j].z << 3) ^ v[j].w);
+                __builtin_nontemporal_store(o, reinterpret_cast<uint32_t *>(
+                                                   out + rr * nc * 4 + (int64_t)c * 4));
+                if ((lane & 1) == 0)
+                    sb[c >> 1] = (uint8_t)v[j].x;
+            } else {
+                const uint2 o = make_uint2((v[j].x >> 8) ^ v[j].y, (v[j].z >> 8) ^ v[j].w);
+                __builtin_nontemporal_store(((unsigned long long)o.y << 32) | o.x,
+                                            reinterpret_cast<unsigned long long *>(
+                                                out + rr * nc * 8 + (int64_t)c * 8));
+                if ((lane & 3) == 0)
+                    sb[c >> 2] = (uint8_t)v[j].x;
+            }
         }
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    const int K = nc / 4;
+    const int K = MODE == MX_STREAM_NVFP4 ? nc / 2 : nc / 4;
     typedef unsigned int u32x4v __attribute__((ext_vector_type(4)));
     if (row_ok && lane < K / 16)
         __builtin_nontemporal_store(*reinterpret_cast<const u32x4v *>(sb + 16 * lane),
@@ -90,7 +99,8 @@ extern "C" int mx_stream_reference(const void *x, int64_t T, int64_t d, uint8_t 
 {
     if (T < 0 || d <= 0 || d % 512 != 0 || d > 4096 || T > ((int64_t)1 << 34))
         return 1;
-    if (mode != MX_STREAM_MIXED && mode != MX_STREAM_READ && mode != MX_STREAM_WRITE)
+    if (mode != MX_STREAM_MIXED && mode != MX_STREAM_READ && mode != MX_STREAM_WRITE &&
+        mode != MX_STREAM_NVFP4)
         return 1;
     if (T == 0)
         return 0;
@@ -105,7 +115,9 @@ extern "C" int mx_stream_reference(const void *x, int64_t T, int64_t d, uint8_t 
         hipLaunchKernelGGL(stream_kernel<MX_STREAM_MIXED>, grid, block, 0, st, xp, T, nc, out, out_small);
     else if (mode == MX_STREAM_READ)
         hipLaunchKernelGGL(stream_kernel<MX_STREAM_READ>, grid, block, 0, st, xp, T, nc, out, out_small);
-    else
+    else if (mode == MX_STREAM_WRITE)
         hipLaunchKernelGGL(stream_kernel<MX_STREAM_WRITE>, grid, block, 0, st, xp, T, nc, out, out_small);
+    else
+        hipLaunchKernelGGL(stream_kernel<MX_STREAM_NVFP4>, grid, block, 0, st, xp, T, nc, out, out_small);
     return hipGetLastError() == hipSuccess ? 0 : 3;
 }

@@ -7,7 +7,7 @@ import os
 import torch
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libstreamref.so")
-MODES = {"mixed": 0, "read": 1, "write": 2}
+MODES = {"mixed": 0, "read": 1, "write": 2, "nvfp4": 3}
 _lib = None
 
 
@@ -26,8 +26,9 @@ def load():
 
 
 def stream_reference(x, out, out_small, mode="mixed"):
-    """x bf16 [T, d] (d % 512 == 0, d <= 4096); out uint8 [T, d]; out_small
-    uint8 [T, d/32] (mixed, write) or [T, 16] (read)."""
+    """x bf16 [T, d] (d % 512 == 0, d <= 4096); out uint8 [T, d] (mixed,
+    write) or [T, d/2] (nvfp4); out_small uint8 [T, d/32] (mixed, write),
+    [T, 16] (read) or [T, d/16] (nvfp4)."""
     T, d = x.shape
     st = load().mx_stream_reference(ctypes.c_void_p(x.data_ptr()), T, d,
                                     ctypes.c_void_p(out.data_ptr()),

@@ -58,3 +58,17 @@ def test_more_than_one_gpu_is_refused():
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2
     assert "one GPU" in r.stderr
+
+
+def test_cpu_baseline_reports_cores_model_and_every_config():
+    import bench
+    from paper_2603_13180_amd import synth
+    w = synth.generate(bench.WORKLOAD, rows=range(512))
+    r = bench.cpu_baseline(w.x, w.preset.d, budget_s=0.05, per_config_s=0.05, parallel_rows=256)
+    assert r["kind"] == "oracle" and r["cores"] == 1 and r["unit"] == "GB/s" and r["value"] > 0
+    assert r["nproc"] >= 1 and r["cores_available"] >= 1 and r["cpu_model"]
+    assert set(r["per_config"]) == {name for name, _ in bench.CPU_CONFIGS}
+    assert set(name for name, _ in bench.CPU_CONFIGS) == set(synth.PRESETS)
+    for v in r["per_config"].values():
+        assert v["rows"] > 0 and v["GB/s"] > 0
+    assert r["row_parallel"]["threads"] >= 1 and r["row_parallel"]["rows"] == 256

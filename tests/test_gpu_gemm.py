@@ -9,6 +9,9 @@ instruction can be dropped.  The test bound is |H - H_oracle| <=
 the exactness test below (at most one product per output) pins the operand
 layout and the scale association bit for bit.
 """
+import os
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
 import pytest
 import torch
@@ -179,3 +182,145 @@ def test_mxnorm_linear_forward(block_elem, T, d, N):
     mag = oracle.mx_matmul(abs_codes(ac, elem), as_, abs_codes(wc_o, elem), ws_o, d, elem=elem)
     assert_close(h.cpu().numpy().astype(np.float64), want, mag, False,
                  "mxnorm_linear %s T=%d d=%d N=%d" % (elem, T, d, N))
+
+
+# ------------------------------------------- the benchmarked shapes --
+#
+# The kernel maps workgroups to 256 x 256 output tiles through an XCD-aware
+# renumbering and visits tile rows in groups of 4.  These tests run it at the
+# Llama-3-8B projection shapes the layer benchmark times (d = 4096; QKV N =
+# 6144, gate+up N = 28672) and at a mid-size shape compared in full, so that
+# several complete groups, the ragged last group and the full K = 4096 loop
+# are checked against the oracle.
+
+WORKERS = max(1, min(16, os.cpu_count() or 1))
+
+
+def oracle_product(ac, as_, bc, bs, K, elem):
+    """(H, sum_k |a b|) of A's rows against B's rows from the oracle, B's rows
+    split over threads (each oracle call runs in C without the GIL)."""
+    oracle.mx_matmul(ac[:1], as_[:1], bc[:1], bs[:1], K, elem=elem)   # load the library once
+    chunks = [c for c in np.array_split(np.arange(bc.shape[0]), WORKERS) if len(c)]
+
+    def one(ix):
+        b, s = bc[ix], bs[ix]
+        return (oracle.mx_matmul(ac, as_, b, s, K, elem=elem),
+                oracle.mx_matmul(abs_codes(ac, elem), as_, abs_codes(b, elem), s, K, elem=elem))
+
+    with ThreadPoolExecutor(len(chunks)) as ex:
+        parts = list(ex.map(one, chunks))
+    return (np.concatenate([p[0] for p in parts], 1), np.concatenate([p[1] for p in parts], 1))
+
+
+def tile_sample(n, tile=256, lead=8, tail=2, extra=14, seed=0):
+    """Indices over n rows (or columns) in 256-wide tiles: the first `lead`
+    tiles (two whole groups of 4 tile rows), the last `tail`, and `extra`
+    random ones; in each, the tile's first and last index and one random."""
+    rng = np.random.default_rng(seed)
+    nt = -(-n // tile)
+    tiles = set(range(min(lead, nt))) | set(range(max(0, nt - tail), nt))
+    rest = sorted(set(range(nt)) - tiles)
+    if rest:
+        tiles |= set(rng.choice(rest, min(extra, len(rest)), replace=False).tolist())
+    idx = set()
+    for t in tiles:
+        lo, hi = t * tile, min(n, (t + 1) * tile) - 1
+        idx |= {lo, hi, int(rng.integers(lo, hi + 1))}
+    return np.array(sorted(idx))
+
+
+def big_operand(rows, K, elem, rng):
+    return random_operand(rows, K, elem, rng)
+
+
+def dev_u8(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+@pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("elem", ELEMS)
+def test_qkv_shape_sampled_rows(elem, out_dtype):
+    # [32768, 4096] x [6144, 4096]^T: 128 x 24 tiles, 3072 workgroups; about
+    # 70 rows from 24 tile rows (both first groups, the last two, random
+    # others), every column
+    M, N, K = 32768, 6144, 4096
+    rng = np.random.default_rng(31 + len(elem))
+    ac, as_ = big_operand(M, K, elem, rng)
+    bc, bs = big_operand(N, K, elem, rng)
+    h = mxnorm.mx_matmul_fwd(dev_u8(ac), dev_u8(as_), dev_u8(bc), dev_u8(bs), K, elem=elem,
+                             out_dtype=out_dtype)
+    rows = tile_sample(M)
+    assert len(rows) >= 64
+    got = h[torch.from_numpy(rows).to(DEV)].float().cpu().numpy().astype(np.float64)
+    want, mag = oracle_product(ac[rows], as_[rows], bc, bs, K, elem)
+    assert_close(got, want, mag, out_dtype == torch.bfloat16,
+                 "qkv %s %s (%d rows)" % (elem, out_dtype, len(rows)))
+
+
+@pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
+def test_gate_up_shape_sampled(out_dtype):
+    # [16384, 4096] x [28672, 4096]^T: 64 x 112 tiles; sampled rows against
+    # sampled columns from 24 tile columns
+    M, N, K, elem = 16384, 28672, 4096, "e4m3"
+    rng = np.random.default_rng(41)
+    ac, as_ = big_operand(M, K, elem, rng)
+    bc, bs = big_operand(N, K, elem, rng)
+    h = mxnorm.mx_matmul_fwd(dev_u8(ac), dev_u8(as_), dev_u8(bc), dev_u8(bs), K, elem=elem,
+                             out_dtype=out_dtype)
+    rows, cols = tile_sample(M, seed=1), tile_sample(N, lead=2, extra=20, seed=2)
+    assert len(rows) >= 64 and len(cols) >= 64
+    sub = h[torch.from_numpy(rows).to(DEV)][:, torch.from_numpy(cols).to(DEV)]
+    got = sub.float().cpu().numpy().astype(np.float64)
+    want, mag = oracle_product(ac[rows], as_[rows], bc[cols], bs[cols], K, elem)
+    assert_close(got, want, mag, out_dtype == torch.bfloat16,
+                 "gate+up %s (%d x %d sampled)" % (out_dtype, len(rows), len(cols)))
+
+
+@pytest.mark.parametrize("elem", ELEMS)
+def test_mid_shape_every_output(elem):
+    # 9 tile rows (two full groups of 4 and a group of 1) x 5 tile columns
+    # (the last one 16 columns wide), K = 4096: every output compared
+    M, N, K = 2304, 1040, 4096
+    rng = np.random.default_rng(51 + len(elem))
+    ac, as_ = random_operand(M, K, elem, rng)
+    bc, bs = random_operand(N, K, elem, rng)
+    for out_dtype in (torch.float32, torch.bfloat16):
+        got = gpu_matmul(ac, as_, bc, bs, K, elem, out_dtype)
+        if out_dtype == torch.float32:
+            want, mag = oracle_product(ac, as_, bc, bs, K, elem)
+        assert_close(got, want, mag, out_dtype == torch.bfloat16,
+                     "mid %s %s every output" % (elem, out_dtype))
+
+
+def test_mxnorm_linear_forward_at_qkv_shape():
+    # the benchmarked MXNormLinear forward: MXNorm of the Llama-3-8B
+    # activations [32768, 4096] (outlier channels), then the product with
+    # MXCast(W gamma) for a QKV weight [6144, 4096]; the activation codes and
+    # scales of the sampled rows are bit-exact and H is within the bound
+    w = synth.generate("llama3-8b-d4096")
+    T, d, N = w.preset.T, w.preset.d, 6144
+    rng = np.random.default_rng(61)
+    wb = synth.f32_to_bf16_bits((rng.standard_normal((N, d)) * 0.02).astype(np.float32))
+    x = torch.from_numpy(w.x.view(np.int16)).to(DEV).view(torch.bfloat16)
+    g = torch.from_numpy(w.gamma.view(np.int16)).to(DEV).view(torch.bfloat16)
+    wt = torch.from_numpy(wb.view(np.int16)).to(DEV).view(torch.bfloat16)
+    wc, ws = mxnorm.mx_cast_fwd(wt, g)
+    codes, scales, rho = mxnorm.mxnorm_mx_fwd(x)
+    h = mxnorm.mx_matmul_fwd(codes, scales, wc, ws, d, out_dtype=torch.bfloat16)
+    rows = tile_sample(T, seed=3)
+    ri = torch.from_numpy(rows).to(DEV)
+    got_h = h[ri].float().cpu().numpy().astype(np.float64)
+    got_c, got_s = codes[ri].cpu().numpy(), scales[ri].cpu().numpy()
+    wcs = wc.cpu().numpy(), ws.cpu().numpy()
+    torch.cuda.synchronize()
+    ac, as_, r32, _ = oracle.mxnorm_mx(w.x[rows])
+    assert np.array_equal(got_c, ac) and np.array_equal(got_s, as_)
+    assert np.array_equal(rho[ri].cpu().numpy(), r32)
+    chunks = [c for c in np.array_split(np.arange(N), WORKERS) if len(c)]
+    with ThreadPoolExecutor(len(chunks)) as ex:
+        parts = list(ex.map(lambda ix: oracle.mxcast_gain(wb[ix], w.gamma), chunks))
+    wc_o = np.concatenate([p[0] for p in parts])
+    ws_o = np.concatenate([p[1] for p in parts])
+    assert np.array_equal(wcs[0], wc_o) and np.array_equal(wcs[1], ws_o)
+    want, mag = oracle_product(ac, as_, wc_o, ws_o, d, "e4m3")
+    assert_close(got_h, want, mag, True, "MXNormLinear qkv (%d rows)" % len(rows))

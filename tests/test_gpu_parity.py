@@ -6,6 +6,9 @@ bit-exact; the per-row inverse RMS (estimate) bit-equal to the oracle's float
 value and within 1e-6 relative of its double value.  Both sides round rho to
 float from a double computation; everything deciding a code is float.
 """
+import os
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
 import pytest
 import torch
@@ -240,46 +243,74 @@ def test_e2m1_ties_through_rmsnorm_nvfp4():
 
 
 # ---------------------------------------------------- full-size presets --
+#
+# Every workload preset at its real shape, in the launch configuration the
+# bench times: every row of the four d <= 4096 presets, and at the
+# [131072, 4096] stress preset 4096 random rows plus every zero and constant
+# row, in both scale modes.  The oracle runs over row chunks on threads (its
+# C calls release the GIL).
 
-def sample_rows(T, extra=(), n=192, seed=0):
-    rng = np.random.default_rng(seed)
-    rows = set(rng.choice(T, min(n, T), replace=False).tolist()) | {0, T - 1} | set(extra)
-    return np.array(sorted(rows))
+WORKERS = max(1, min(16, os.cpu_count() or 1))
+
+
+def oracle_rows(fn, x, *args, **kw):
+    """fn(x, ...) -> (codes, scales, rho32, rho64), computed over contiguous
+    row chunks of x on WORKERS threads and joined."""
+    fn(x[:1], *args, **kw)  # load the library before the threads start
+    chunks = [c for c in np.array_split(np.arange(len(x)), 4 * WORKERS) if len(c)]
+    with ThreadPoolExecutor(WORKERS) as ex:
+        parts = list(ex.map(lambda ix: fn(x[ix[0]:ix[-1] + 1], *args, **kw), chunks))
+    return tuple(np.concatenate([p[i] for p in parts]) for i in range(4))
+
+
+def gpu_rows(out, rows=None):
+    if rows is None:
+        return tuple(t.cpu().numpy() for t in out)
+    ri = torch.from_numpy(rows).to(DEV)
+    return tuple(t[ri].cpu().numpy() for t in out)
+
+
+def check_preset(w, x, g, xs, rows, modes, name):
+    T, d = w.preset.T, w.preset.d
+    if w.preset.fmt == "mxfp8":
+        for mode in modes:
+            got = gpu_rows(mxnorm.mxnorm_mxfp8_fwd(x, scale_mode=mode), rows)
+            assert_parity("mxnorm_mxfp8", got, oracle_rows(oracle.mxnorm_mxfp8, xs, mode=mode),
+                          name + " " + mode)
+            got = gpu_rows(mxnorm.rmsnorm_mxfp8_fwd(x, g, scale_mode=mode), rows)
+            assert_parity("rmsnorm_mxfp8", got,
+                          oracle_rows(oracle.rmsnorm_mxfp8, xs, w.gamma, mode=mode),
+                          name + " " + mode)
+    else:
+        s_g = sg_mxnorm(d)
+        got = gpu_rows(mxnorm.mxnorm_nvfp4_fwd(x, s_g), rows)
+        assert_parity("mxnorm_nvfp4", got, oracle_rows(oracle.mxnorm_nvfp4, xs, s_g), name)
+        s_r = sg_rmsnorm(d, w.gamma)
+        got = gpu_rows(mxnorm.rmsnorm_nvfp4_fwd(x, g, s_r), rows)
+        assert_parity("rmsnorm_nvfp4", got, oracle_rows(oracle.rmsnorm_nvfp4, xs, s_r, w.gamma),
+                      name)
 
 
 @pytest.mark.parametrize("name", ["llama3-125m-d768", "llama3-1b-d2048", "llama3-8b-d4096",
-                                  "llama3-8b-d4096-nvfp4", "llama3-8b-longctx-stress"])
-def test_full_size_presets_sampled(name):
+                                  "llama3-8b-d4096-nvfp4"])
+def test_full_size_presets_every_row(name):
+    w = synth.generate(name)
+    check_preset(w, dev_bf16(w.x), dev_bf16(w.gamma), w.x, None, ("rceil", "floor"), name)
+
+
+def test_stress_preset_every_zero_and_constant_row():
+    name = "llama3-8b-longctx-stress"
     w = synth.generate(name)
     P = w.preset
-    x = dev_bf16(w.x)
-    g = dev_bf16(w.gamma)
-    T, d = P.T, P.d
-    extra = ()
-    if P.kind == "t3_stress":
-        aux = synth._aux(P, 0)
-        extra = list(aux["zero_rows"][:8]) + list(aux["const_rows"][:8])
-    rows = sample_rows(T, extra)
-    xs = w.x[rows]
-    if P.fmt == "mxfp8":
-        modes = ("rceil", "floor") if P.kind == "t3_stress" else ("rceil",)
-        for mode in modes:
-            out = mxnorm.mxnorm_mxfp8_fwd(x, scale_mode=mode)
-            got = tuple(t.cpu().numpy()[rows] for t in out)
-            assert_parity("mxnorm_mxfp8", got, oracle.mxnorm_mxfp8(xs, mode=mode), name + mode)
-            out = mxnorm.rmsnorm_mxfp8_fwd(x, g, scale_mode=mode)
-            got = tuple(t.cpu().numpy()[rows] for t in out)
-            assert_parity("rmsnorm_mxfp8", got, oracle.rmsnorm_mxfp8(xs, w.gamma, mode=mode),
-                          name + mode)
-    else:
-        s_g = sg_mxnorm(d)
-        out = mxnorm.mxnorm_nvfp4_fwd(x, s_g)
-        got = tuple(t.cpu().numpy()[rows] for t in out)
-        assert_parity("mxnorm_nvfp4", got, oracle.mxnorm_nvfp4(xs, s_g), name)
-        s_r = sg_rmsnorm(d, w.gamma)
-        out = mxnorm.rmsnorm_nvfp4_fwd(x, g, s_r)
-        got = tuple(t.cpu().numpy()[rows] for t in out)
-        assert_parity("rmsnorm_nvfp4", got, oracle.rmsnorm_nvfp4(xs, s_r, w.gamma), name)
+    aux = synth._aux(P, 0)
+    zero, const = np.asarray(aux["zero_rows"]), np.asarray(aux["const_rows"])
+    assert len(zero) == len(const) == P.T // 100
+    rng = np.random.default_rng(7)
+    rows = np.array(sorted(set(rng.choice(P.T, 4096, replace=False).tolist())
+                           | set(zero.tolist()) | set(const.tolist()) | {0, P.T - 1}))
+    xs = np.ascontiguousarray(w.x[rows])
+    assert (xs[np.searchsorted(rows, zero)] & 0x7FFF == 0).all()
+    check_preset(w, dev_bf16(w.x), dev_bf16(w.gamma), xs, rows, ("rceil", "floor"), name)
 
 
 # ------------------------------------------------------- buffer hygiene --
