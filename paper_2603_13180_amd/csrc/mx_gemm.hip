@@ -10,19 +10,28 @@
 // each operand with one scale byte per row and 32-element block applied
 // exactly, accumulating in fp32.
 //
-// Tiling: a workgroup of 4 waves computes a 256 (M) x 256 (N) tile; each wave
-// a 128 x 128 quarter as 8 x 8 matrix-core tiles of 16 x 16, accumulated in
-// the AGPRs.  The K loop moves 128 bytes of every row per step (128 E4M3 or
-// 256 E2M1 elements) from global memory straight into LDS (16-byte
-// global_load_lds, no staging registers), double-buffered, and reads the next
-// step's fragments into registers while the current step's matrix-core work
-// runs (see the pipeline note in the kernel).  In LDS, 16-byte chunk c of row r lives at chunk
-// c ^ (r & 7) of the row, so the fragment reads of 8 consecutive rows hit
-// distinct banks.  Workgroups are renumbered so that each XCD (each with its
-// own L2) runs a contiguous range of tiles, visited in groups of tile rows
-// that share operand blocks.
+// Tiling: a workgroup of 8 waves (two per SIMD) computes a 256 (M) x 256 (N)
+// output tile; wave w owns the 128 x 64 quarter-column (w & 1, w >> 1) as
+// 8 x 4 matrix-core tiles of 16 x 16, 128 accumulator registers.  Two waves
+// per SIMD are what lets the matrix core run while the other wave waits on
+// LDS or a barrier: with one wave per SIMD the E2M1 instruction issues at
+// about half its rate.  The K loop moves 128 bytes of every row per step
+// (128 E4M3 or 256 E2M1 elements) from global memory straight into LDS
+// (16-byte global_load_lds, no staging registers) into two stages of 66 KB;
+// each step reads its four B fragments into registers and streams the eight
+// A fragments two ahead of the matrix core.  In LDS, 16-byte chunk c of row r
+// lives at chunk c ^ (r & 7) of the row, so the fragment reads of 8
+// consecutive rows hit distinct banks.
+//
+// What bounds it: at 256 x 256 the operand stream is 64 KB per K step per
+// workgroup, about 10 TB/s of 64-byte L2 requests at half the fp8 peak, and
+// the L2 channels are busy ~94% of the kernel's time (rocprofv3 TCC_BUSY at
+// the QKV shape).  The register file holds at most about this output tile
+// (its accumulators are half of it), and LDS at most two stages of it.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include <type_traits>
 
 #include "mxnorm.h"
 #include "status.h"
@@ -31,14 +40,15 @@ namespace mxg {
 
 typedef int v8i __attribute__((ext_vector_type(8)));
 typedef float v4f __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 #define LDS_AS __attribute__((address_space(3)))
 
 constexpr int BM = 256;    // tile rows of A (M)
 constexpr int BN = 256;    // tile rows of B (N)
 constexpr int KB = 128;    // bytes of each row per K step
-constexpr int NT = 256;    // threads: 4 waves
+constexpr int NT = 512;    // threads: 8 waves, two per SIMD
 constexpr int WTM = 128;   // wave tile along M
-constexpr int WTN = 128;   // wave tile along N
+constexpr int WTN = 64;    // wave tile along N
 constexpr int FM = WTM / 16, FN = WTN / 16;
 constexpr int GROUP_M = 4; // tile rows per group in the visiting order
 constexpr int NXCD = 8;
@@ -46,7 +56,6 @@ constexpr int NXCD = 8;
 // scale bytes per row and K step: 4 blocks of 32 (E4M3), 8 blocks (E2M1)
 template <int ELEM> struct Op {
     static constexpr int SB = ELEM == MX_ELEM_E2M1 ? 8 : 4;
-    static constexpr int FMT = ELEM == MX_ELEM_E2M1 ? 4 : 0; // matrix-core operand format
     static constexpr int STAGE = (BM + BN) * KB + (BM + BN) * SB;
 };
 
@@ -59,6 +68,7 @@ struct Args {
     int64_t rs;   // scale bytes per row
     int steps;    // K steps of KB bytes
     int tiles_m, tiles_n;
+    int xcd_ranges; // 1: each XCD runs a contiguous range of tiles; 0: round robin
 };
 
 // Global -> LDS DMA loads: lane i of the wave reads gbase + off_i (gbase
@@ -84,20 +94,32 @@ __device__ __forceinline__ void lds_load4(const void *gbase, uint32_t off, uint3
                  : "memory");
 }
 
-// Wait until at most N of this wave's vector memory loads are outstanding
-// (they complete in issue order).
-template <int N> __device__ __forceinline__ void wait_vmcnt()
+// Wait until none of this wave's vector memory loads is outstanding.
+__device__ __forceinline__ void wait_vmcnt0() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Workgroup barrier without the memory fence of __syncthreads(): the fence
+// would wait for every outstanding load, including the DMA of the next step.
+// LDS written by the DMA is covered by the vmcnt wait each wave makes before
+// arriving; the lgkmcnt(0) completes this wave's own LDS reads, so that a
+// stage read before the barrier can be refilled after it.  The "memory"
+// clobber keeps the compiler from moving LDS accesses across it.
+__device__ __forceinline__ void barrier()
 {
-    static_assert(N >= 0 && N < 64, "vmcnt range");
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
 // Per-lane part of the DMA addresses, fixed for the whole K loop: byte
 // offsets, relative to the tile's first row, of the rows this lane moves.
-// Rows past M or N read row M-1 or N-1: their results are never stored.
+// Wave w moves code rows 32w .. 32w+31 of both tiles (4 instructions of
+// 8 rows x 128 bytes each: lane l fills LDS slot l % 8 of row l / 8 of its
+// group, which holds source chunk (l % 8) ^ (l / 8)); waves 0-3 move the
+// scale bytes of A's rows 64w .. 64w+63, waves 4-7 those of B's rows
+// 64(w-4) .. 64(w-4)+63 (lane i of scale instruction u moves dword
+// i % (SB/4) of row u (64 / (SB/4)) + i / (SB/4)).  Rows past M or N read
+// row M-1 or N-1: their results are never stored.
 template <int ELEM> struct Rows {
-    uint32_t a[8], b[8];     // code rows 64w + 8t + l/8, times the row pitch, plus the chunk
-    uint32_t sa[Op<ELEM>::SB / 4], sb[Op<ELEM>::SB / 4]; // scale rows, plus the dword
+    uint32_t a[4], b[4];
+    uint32_t s[Op<ELEM>::SB / 4];
 };
 
 template <int ELEM>
@@ -106,29 +128,26 @@ __device__ __forceinline__ Rows<ELEM> lane_rows(const Args &A, int64_t m0, int64
 {
     constexpr int DW = Op<ELEM>::SB / 4;
     Rows<ELEM> R;
-    const int rr = l >> 3;        // row within the 8-row group
-    const int ch = (l & 7) ^ rr;  // source chunk for this LDS slot (the swizzle)
+    const int rr = l >> 3;       // row within the 8-row group
+    const int ch = (l & 7) ^ rr; // source chunk for this LDS slot (the swizzle)
 #pragma unroll
-    for (int t = 0; t < 8; ++t) {
-        const int r = 64 * w + 8 * t + rr;
+    for (int t = 0; t < 4; ++t) {
+        const int r = 32 * w + 8 * t + rr;
         R.a[t] = (uint32_t)((min(m0 + r, A.M - 1) - m0) * A.rb) + 16 * ch;
         R.b[t] = (uint32_t)((min(n0 + r, A.N - 1) - n0) * A.rb) + 16 * ch;
     }
+    const bool on_a = w < 4;
+    const int64_t base = on_a ? m0 : n0, lim = on_a ? A.M : A.N;
 #pragma unroll
     for (int u = 0; u < DW; ++u) {
-        const int r = 64 * w + u * (64 / DW) + l / DW;
-        R.sa[u] = (uint32_t)((min(m0 + r, A.M - 1) - m0) * A.rs) + 4 * (l % DW);
-        R.sb[u] = (uint32_t)((min(n0 + r, A.N - 1) - n0) * A.rs) + 4 * (l % DW);
+        const int r = 64 * (w & 3) + u * (64 / DW) + l / DW;
+        R.s[u] = (uint32_t)((min(base + r, lim - 1) - base) * A.rs) + 4 * (l % DW);
     }
     return R;
 }
 
-// Issue the loads of K step s into one LDS stage.  Wave w moves rows
-// 64w .. 64w+63 of both operand tiles (8 instructions of 8 rows x 128 bytes
-// each; lane l fills LDS slot l of its group, which holds source chunk
-// (l % 8) ^ (l / 8)) and their scale bytes, stored row-major [row][SB]
-// (lane i of scale instruction u moves dword i % (SB/4) of row
-// 64w + u (64 / (SB/4)) + i / (SB/4)).
+// Issue this wave's loads of K step s into one LDS stage, laid out as
+// [A codes 256 x 128][B codes 256 x 128][A scales 256 x SB][B scales 256 x SB].
 template <int ELEM>
 __device__ __forceinline__ void issue_step(const uint8_t *ta, const uint8_t *tb,
                                            const uint8_t *tsa, const uint8_t *tsb,
@@ -138,41 +157,17 @@ __device__ __forceinline__ void issue_step(const uint8_t *ta, const uint8_t *tb,
     constexpr int DW = SB / 4;
     const uint32_t xa = stage;
     const uint32_t xb = stage + BM * KB;
-    const uint32_t sa = stage + (BM + BN) * KB;
-    const uint32_t sb = sa + BM * SB;
     const uint32_t kc = (uint32_t)s * KB, ks = (uint32_t)s * SB;
 #pragma unroll
-    for (int t = 0; t < 8; ++t) {
-        lds_load16(ta, R.a[t] + kc, xa + (64 * w + 8 * t) * KB);
-        lds_load16(tb, R.b[t] + kc, xb + (64 * w + 8 * t) * KB);
+    for (int t = 0; t < 4; ++t) {
+        lds_load16(ta, R.a[t] + kc, xa + (32 * w + 8 * t) * KB);
+        lds_load16(tb, R.b[t] + kc, xb + (32 * w + 8 * t) * KB);
     }
+    const uint8_t *ts = w < 4 ? tsa : tsb;
+    const uint32_t xs = stage + (BM + BN) * KB + (w < 4 ? 0 : BM * SB) + 64 * (w & 3) * SB;
 #pragma unroll
-    for (int u = 0; u < DW; ++u) {
-        lds_load4(tsa, R.sa[u] + ks, sa + (64 * w + u * (64 / DW)) * SB);
-        lds_load4(tsb, R.sb[u] + ks, sb + (64 * w + u * (64 / DW)) * SB);
-    }
-}
-
-// Workgroup barrier without the memory fence of __syncthreads(): the fence
-// would wait for every outstanding load, including the prefetch of the next
-// step.  LDS written by the DMA loads is covered by the explicit vmcnt waits
-// each wave makes before arriving; the lgkmcnt(0) completes this wave's own
-// LDS reads, so that a stage read before the barrier can be refilled after
-// it.  The "memory" clobber keeps the compiler from moving LDS accesses
-// across it.
-__device__ __forceinline__ void barrier()
-{
-    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-}
-
-// loads per lane in issue_step
-template <int ELEM> constexpr int loads_per_step() { return 16 + 2 * (Op<ELEM>::SB / 4); }
-
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ u32x4 lds_chunk(const LDS_AS uint8_t *base, int row, int c)
-{
-    return *reinterpret_cast<const LDS_AS u32x4 *>(base + row * KB + 16 * (c ^ (row & 7)));
+    for (int u = 0; u < DW; ++u)
+        lds_load4(ts, R.s[u] + ks, xs + u * (64 / DW) * SB);
 }
 
 __device__ __forceinline__ v8i join(u32x4 lo, u32x4 hi)
@@ -180,12 +175,13 @@ __device__ __forceinline__ v8i join(u32x4 lo, u32x4 hi)
     return __builtin_bit_cast(v8i, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
-__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f)
+// two floats to bf16 (round to nearest even, on gfx950's conversion unit),
+// the first in the low half
+__device__ __forceinline__ uint32_t pack_bf16(float a, float b)
 {
-    const uint32_t u = __float_as_uint(f);
-    if ((u & 0x7FFFFFFFu) > 0x7F800000u)
-        return (uint16_t)((u >> 16) | 0x40u); // quiet NaN, sign kept
-    return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+    const __bf16 x = (__bf16)a, y = (__bf16)b;
+    return (uint32_t)__builtin_bit_cast(uint16_t, x) |
+           ((uint32_t)__builtin_bit_cast(uint16_t, y) << 16);
 }
 
 // One operand fragment for a 16-row group and one K step: lane (g, q) holds
@@ -199,22 +195,38 @@ struct Frag {
     int s0, s1;
 };
 
+// Lane-relative LDS offsets of one operand's fragments within a stage: the
+// lane reads row r0 + qd (+16 j for fragment j) at chunks g and 4 + g,
+// swizzled by (r0 + qd) & 7 = qd & 7 (r0 is a multiple of 16), and the
+// scale bytes g (and 4 + g) of that row.
+struct FragBase {
+    uint32_t lo, hi, sc;
+};
+
 template <int ELEM>
-__device__ __forceinline__ Frag read_frag(const LDS_AS uint8_t *codes,
-                                          const LDS_AS uint8_t *scales, int r, int g)
+__device__ __forceinline__ FragBase frag_base(uint32_t codes_off, uint32_t scales_off, int r0,
+                                              int qd, int g)
 {
+    constexpr int SB = Op<ELEM>::SB;
+    FragBase b;
+    b.lo = codes_off + (r0 + qd) * KB + 16 * (g ^ (qd & 7));
+    b.hi = codes_off + (r0 + qd) * KB + 16 * ((4 + g) ^ (qd & 7));
+    b.sc = scales_off + (r0 + qd) * SB + g;
+    return b;
+}
+
+// fragment J of an operand from the stage at st; the row offset J*16 rows is
+// a compile-time constant that the LDS reads take as their immediate offset
+template <int ELEM, int J>
+__device__ __forceinline__ Frag read_frag(const LDS_AS uint8_t *st, const FragBase &b)
+{
+    constexpr int SB = Op<ELEM>::SB;
     Frag f;
-    f.v = join(lds_chunk(codes, r, g), lds_chunk(codes, r, 4 + g));
-    if constexpr (ELEM == MX_ELEM_E2M1) {
-        typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
-        const u32x2 d = *reinterpret_cast<const LDS_AS u32x2 *>(scales + r * 8);
-        f.s0 = (int)((d.x >> (8 * g)) & 0xFFu);
-        f.s1 = (int)((d.y >> (8 * g)) & 0xFFu);
-    } else {
-        const uint32_t d = *reinterpret_cast<const LDS_AS uint32_t *>(scales + r * 4);
-        f.s0 = (int)((d >> (8 * g)) & 0xFFu);
-        f.s1 = 0;
-    }
+    const u32x4 lo = *reinterpret_cast<const LDS_AS u32x4 *>(st + b.lo + J * 16 * KB);
+    const u32x4 hi = *reinterpret_cast<const LDS_AS u32x4 *>(st + b.hi + J * 16 * KB);
+    f.v = join(lo, hi);
+    f.s0 = st[b.sc + J * 16 * SB];
+    f.s1 = ELEM == MX_ELEM_E2M1 ? (int)st[b.sc + J * 16 * SB + 4] : 0;
     return f;
 }
 
@@ -244,13 +256,18 @@ __global__ void __launch_bounds__(NT) mx_gemm_kernel(Args A)
     constexpr int STAGE = Op<ELEM>::STAGE;
     __shared__ __attribute__((aligned(16))) uint8_t lds[2 * STAGE];
 
-    // tile of this workgroup: contiguous per XCD (dispatch is round-robin
-    // over the XCDs), then grouped GROUP_M tile rows at a time
+    // tile of this workgroup.  Dispatch is round robin over the XCDs (each
+    // with its own L2).  With xcd_ranges the workgroups are renumbered so
+    // that each XCD runs a contiguous range of tiles; either way the tiles
+    // are visited in groups of GROUP_M tile rows that share operand blocks.
     const int G = A.tiles_m * A.tiles_n;
     const int wg = blockIdx.x;
-    const int xcd = wg % NXCD, loc = wg / NXCD;
-    const int q = G / NXCD, rem = G % NXCD;
-    const int pid = xcd < rem ? xcd * (q + 1) + loc : rem * (q + 1) + (xcd - rem) * q + loc;
+    int pid = wg;
+    if (A.xcd_ranges) {
+        const int xcd = wg % NXCD, loc = wg / NXCD;
+        const int q = G / NXCD, rem = G % NXCD;
+        pid = xcd < rem ? xcd * (q + 1) + loc : rem * (q + 1) + (xcd - rem) * q + loc;
+    }
     const int in_group = GROUP_M * A.tiles_n;
     const int first_m = (pid / in_group) * GROUP_M;
     const int gsz = min(A.tiles_m - first_m, GROUP_M);
@@ -271,90 +288,54 @@ __global__ void __launch_bounds__(NT) mx_gemm_kernel(Args A)
         for (int j = 0; j < FM; ++j)
             acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
 
-    // Pipeline.  Registers hold every fragment of the current step.  Each
-    // step is split at a barrier: the first half multiplies A fragments
-    // 0..FM/2-1 with all B fragments; at the barrier the next step's data has
-    // landed in the other stage and every wave has finished reading this
-    // stage, so the DMA for two steps ahead can refill it; the second half
-    // multiplies A fragments FM/2.. fragment by fragment of B, reloading each
-    // B fragment (and the free A fragments) with the next step's data as soon
-    // as it is used up.  A wave therefore never waits on LDS at a step start.
-    constexpr int HJ = FM / 2;
     LDS_AS uint8_t *st0 = (LDS_AS uint8_t *)lds;
     const uint32_t st0_addr = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)st0);
-    auto codes_a = [&](int stage) { return (const LDS_AS uint8_t *)(st0 + stage * STAGE); };
-    auto codes_b = [&](int stage) { return (const LDS_AS uint8_t *)(st0 + stage * STAGE + BM * KB); };
-    auto scales_a = [&](int stage) {
-        return (const LDS_AS uint8_t *)(st0 + stage * STAGE + (BM + BN) * KB);
-    };
-    auto scales_b = [&](int stage) {
-        return (const LDS_AS uint8_t *)(st0 + stage * STAGE + (BM + BN) * KB + BM * SB);
-    };
-
-    // tile bases (wave-uniform) and this lane's row offsets
     const uint8_t *ta = A.a + m0 * A.rb, *tb = A.b + n0 * A.rb;
     const uint8_t *tsa = A.as + m0 * A.rs, *tsb = A.bs + n0 * A.rs;
     const Rows<ELEM> R = lane_rows<ELEM>(A, m0, n0, w, l);
+    const FragBase ba = frag_base<ELEM>(0, (BM + BN) * KB, wm, qd, g);
+    const FragBase bb = frag_base<ELEM>(BM * KB, (BM + BN) * KB + BM * SB, wn, qd, g);
 
+    // Pipeline, one barrier per K step.  At the top of step s every wave has
+    // its own DMA of step s landed (vmcnt) and, past the barrier, so has every
+    // other wave, and no wave still reads the other stage (step s-1): the DMA
+    // of step s+1 goes there.  The step then reads its four B fragments and
+    // streams the eight A fragments, each requested two ahead of the
+    // products that use it.
     issue_step<ELEM>(ta, tb, tsa, tsb, R, 0, st0_addr, w);
-    if (A.steps > 1) {
-        issue_step<ELEM>(ta, tb, tsa, tsb, R, 1, st0_addr + STAGE, w);
-        wait_vmcnt<loads_per_step<ELEM>()>();
-    } else {
-        wait_vmcnt<0>();
-    }
-    barrier();
-
-    Frag fb[FN], fa[FM];
-#pragma unroll
-    for (int i = 0; i < FN; ++i)
-        fb[i] = read_frag<ELEM>(codes_b(0), scales_b(0), wn + 16 * i + qd, g);
-#pragma unroll
-    for (int j = 0; j < FM; ++j)
-        fa[j] = read_frag<ELEM>(codes_a(0), scales_a(0), wm + 16 * j + qd, g);
-
     for (int s = 0; s < A.steps; ++s) {
-        const int cur = s & 1, nxt = cur ^ 1;
-        const bool more = s + 1 < A.steps;
-
-        // every wave has read this step's fragments (during the previous
-        // step): the stage can take the DMA for two steps ahead now
+        const int cur = s & 1;
+        wait_vmcnt0();
         barrier();
-        if (s + 2 < A.steps)
-            issue_step<ELEM>(ta, tb, tsa, tsb, R, s + 2, st0_addr + cur * STAGE, w);
-
-#pragma unroll
-        for (int j = 0; j < HJ; ++j)
+        if (s + 1 < A.steps)
+            issue_step<ELEM>(ta, tb, tsa, tsb, R, s + 1, st0_addr + (cur ^ 1) * STAGE, w);
+        const LDS_AS uint8_t *st = st0 + cur * STAGE;
+        Frag fb[FN], fa[FM];
+        fb[0] = read_frag<ELEM, 0>(st, bb);
+        fb[1] = read_frag<ELEM, 1>(st, bb);
+        fb[2] = read_frag<ELEM, 2>(st, bb);
+        fb[3] = read_frag<ELEM, 3>(st, bb);
+        fa[0] = read_frag<ELEM, 0>(st, ba);
+        fa[1] = read_frag<ELEM, 1>(st, ba);
+        auto column = [&](auto jc) {
+            constexpr int j = decltype(jc)::value;
+            if constexpr (j + 2 < FM)
+                fa[j + 2] = read_frag<ELEM, j + 2>(st, ba);
+            // keep the read ahead of this fragment's products
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int i = 0; i < FN; ++i)
                 mma<ELEM>(acc[i][j], fb[i], fa[j]);
-
-        // the next step's data has landed (the step after it may still be
-        // in flight)
-        if (s + 2 < A.steps)
-            wait_vmcnt<loads_per_step<ELEM>()>();
-        else if (more)
-            wait_vmcnt<0>();
-        barrier();
-
-        // (the reloads are unconditional: after the last step they read a
-        // stale stage that nothing uses, which keeps the loop free of
-        // branches that would hold old and new fragments live together)
-#pragma unroll
-        for (int j = 0; j < HJ; ++j)
-            fa[j] = read_frag<ELEM>(codes_a(nxt), scales_a(nxt), wm + 16 * j + qd, g);
-#pragma unroll
-        for (int i = 0; i < FN; ++i) {
-#pragma unroll
-            for (int j = HJ; j < FM; ++j)
-                mma<ELEM>(acc[i][j], fb[i], fa[j]);
-            // keep the reload after the last use of fb[i] (its registers)
             __builtin_amdgcn_sched_barrier(0);
-            fb[i] = read_frag<ELEM>(codes_b(nxt), scales_b(nxt), wn + 16 * i + qd, g);
-        }
-#pragma unroll
-        for (int j = HJ; j < FM; ++j)
-            fa[j] = read_frag<ELEM>(codes_a(nxt), scales_a(nxt), wm + 16 * j + qd, g);
+        };
+        column(std::integral_constant<int, 0>{});
+        column(std::integral_constant<int, 1>{});
+        column(std::integral_constant<int, 2>{});
+        column(std::integral_constant<int, 3>{});
+        column(std::integral_constant<int, 4>{});
+        column(std::integral_constant<int, 5>{});
+        column(std::integral_constant<int, 6>{});
+        column(std::integral_constant<int, 7>{});
     }
 
     // lane (g, qd) of tile (i, j) holds H[m][n .. n+3] with
@@ -404,8 +385,8 @@ __global__ void __launch_bounds__(NT) mx_gemm_kernel(Args A)
 #pragma unroll
                 for (int h = 0; h < 2; ++h) {
                     const v4f v = gained(i + h, j);
-                    lo[h] = f32_to_bf16_rne(v[0]) | ((uint32_t)f32_to_bf16_rne(v[1]) << 16);
-                    hi[h] = f32_to_bf16_rne(v[2]) | ((uint32_t)f32_to_bf16_rne(v[3]) << 16);
+                    lo[h] = pack_bf16(v[0], v[1]);
+                    hi[h] = pack_bf16(v[2], v[3]);
                 }
                 const auto sl = __builtin_amdgcn_permlane16_swap(lo[0], lo[1], false, false);
                 const auto sh = __builtin_amdgcn_permlane16_swap(hi[0], hi[1], false, false);
@@ -484,6 +465,11 @@ mx_status mx_matmul_fwd(const uint8_t *a_codes, const uint8_t *a_scales, const u
     A.steps = (int)(A.rb / mxg::KB);
     A.tiles_m = (int)tm;
     A.tiles_n = (int)tn;
+    // Tile order, measured at d = 4096 on MI355X: contiguous tile ranges per
+    // XCD are faster up to N = 8192 (the QKV shape: 737 vs 801 us), plain
+    // round robin from N = 16384 on (the gate+up shape, N = 28672: 1765 vs
+    // 1842 us at M = 16384, and likewise at M = 4096 .. 32768).
+    A.xcd_ranges = tn < 64 ? 1 : 0;
     hipStream_t st = static_cast<hipStream_t>(stream);
     hipError_t e;
     if (elem == MX_ELEM_E4M3)

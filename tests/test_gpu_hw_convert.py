@@ -37,6 +37,8 @@ def hwc():
         f.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint32,
                       ctypes.c_void_p]
         f.restype = ctypes.c_int
+    lib.hwc_bf16.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
+    lib.hwc_bf16.restype = ctypes.c_int
     return lib
 
 
@@ -106,7 +108,49 @@ def test_e2m1_conversion_every_input(hwc, e):
     assert n > 50_000_000 if e != -127 else n > 8_000_000
 
 
+def _bf16_rne_bits(u):
+    """float -> bf16 by round to nearest, ties to even, written on the bits:
+    add half a bf16 ulp less one, plus the lowest kept bit, then truncate
+    (a carry into the exponent is the correct rounding up, up to Inf)."""
+    u = u.astype(np.uint64)
+    return (((u + 0x7FFF + ((u >> 16) & 1)) >> 16) & 0xFFFF).astype(np.uint16)
+
+
+def test_bf16_conversion_on_every_rounding_case(hwc):
+    # every upper half-word (sign, exponent, the 7 kept mantissa bits) with
+    # the lower halves that decide the rounding (0, just above 0, just below
+    # and at the tie, just above it, all ones) and random ones; then every
+    # lower half under the upper halves of 1.0, the fp32 subnormals, the
+    # smallest normal and the largest finite values
+    rng = np.random.default_rng(3)
+    hi = np.arange(1 << 16, dtype=np.uint32)
+    lows = np.concatenate([[0x0000, 0x0001, 0x3FFF, 0x7FFF, 0x8000, 0x8001, 0xBFFF, 0xFFFF],
+                           rng.integers(0, 1 << 16, 8)]).astype(np.uint32)
+    u1 = ((hi[:, None] << 16) | lows[None, :]).ravel()
+    every_low = np.arange(1 << 16, dtype=np.uint32)
+    u2 = np.concatenate([(h << 16) | every_low for h in
+                         (0x3F80, 0x0000, 0x8000, 0x0080, 0x7F7F, 0xFF7F, 0x4B12)])
+    u = np.concatenate([u1, u2]).astype(np.uint32)
+    dev = torch.device("cuda:0")
+    x = torch.from_numpy(u.view(np.int32)).to(dev).view(torch.float32)
+    out = torch.empty(u.size, dtype=torch.int16, device=dev)
+    assert hwc.hwc_bf16(x.data_ptr(), out.data_ptr(), u.size,
+                        torch.cuda.current_stream().cuda_stream) == 0
+    got = out.cpu().numpy().view(np.uint16)
+    nan_in = (u & 0x7FFFFFFF) > 0x7F800000
+    want = _bf16_rne_bits(u)
+    bad = np.nonzero((got != want) & ~nan_in)[0]
+    if bad.size:
+        i = bad[0]
+        raise AssertionError("%d of %d differ, first %#010x: got %#06x want %#06x"
+                             % (bad.size, u.size, u[i], got[i], want[i]))
+    # NaN in, NaN out
+    g = got[nan_in]
+    assert ((g & 0x7F80) == 0x7F80).all() and ((g & 0x7F) != 0).all()
+
+
 def test_bad_arguments_launch_nothing(hwc):
     assert hwc.hwc_e4m3(None, None, 3, 127, None) == -1      # odd n
     assert hwc.hwc_e2m1(None, None, 2, 255, None) == -1      # NaN scale byte
     assert hwc.hwc_e4m3(None, None, 0, 127, None) == 0       # empty
+    assert hwc.hwc_bf16(None, None, 5, None) == -1
