@@ -31,6 +31,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
 #include <type_traits>
 
 #include "mxnorm.h"
@@ -69,6 +70,7 @@ struct Args {
     int steps;    // K steps of KB bytes
     int tiles_m, tiles_n;
     int xcd_ranges; // 1: each XCD runs a contiguous range of tiles; 0: round robin
+    int grid_max;   // workgroups resident at once: one per compute unit
 };
 
 // Global -> LDS DMA loads: lane i of the wave reads gbase + off_i (gbase
@@ -230,6 +232,31 @@ __device__ __forceinline__ Frag read_frag(const LDS_AS uint8_t *st, const FragBa
     return f;
 }
 
+// E2M1: one half of a fragment (H = 0: chunk g, block g; H = 1: chunk 4 + g,
+// block 4 + g), the operand of one matrix-core instruction
+struct Half {
+    u32x4 v;
+    int s;
+};
+
+template <int J, int H>
+__device__ __forceinline__ Half read_half(const LDS_AS uint8_t *st, const FragBase &b)
+{
+    constexpr int SB = Op<MX_ELEM_E2M1>::SB;
+    Half f;
+    f.v = *reinterpret_cast<const LDS_AS u32x4 *>(st + (H ? b.hi : b.lo) + J * 16 * KB);
+    f.s = st[b.sc + J * 16 * SB + 4 * H];
+    return f;
+}
+
+__device__ __forceinline__ void mma_half(v4f &acc, const Half &b, const Half &a)
+{
+    const u32x4 z = {0u, 0u, 0u, 0u};
+    const v8i bv = __builtin_bit_cast(v8i, __builtin_shufflevector(b.v, z, 0, 1, 2, 3, 4, 5, 6, 7));
+    const v8i av = __builtin_bit_cast(v8i, __builtin_shufflevector(a.v, z, 0, 1, 2, 3, 4, 5, 6, 7));
+    acc = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(bv, av, acc, 4, 4, 0, b.s, 0, a.s);
+}
+
 // acc += B-fragment x A-fragment over one K step (B is the instruction's
 // first operand: each lane's four results are then four consecutive columns
 // of one row of H)
@@ -249,95 +276,84 @@ __device__ __forceinline__ void mma(v4f &acc, const Frag &b, const Frag &a)
     }
 }
 
-template <int ELEM, int OUT>
-__global__ void __launch_bounds__(NT) mx_gemm_kernel(Args A)
+// The products of one K step from the stage at st: the step's four B
+// fragments held in registers, the eight A fragments streamed, each requested
+// two ahead of the products that use it.
+template <int ELEM>
+__device__ __forceinline__ void step_products(v4f (&acc)[FN][FM], const LDS_AS uint8_t *st,
+                                              const FragBase &ba, const FragBase &bb)
 {
-    constexpr int SB = Op<ELEM>::SB;
-    constexpr int STAGE = Op<ELEM>::STAGE;
-    __shared__ __attribute__((aligned(16))) uint8_t lds[2 * STAGE];
-
-    // tile of this workgroup.  Dispatch is round robin over the XCDs (each
-    // with its own L2).  With xcd_ranges the workgroups are renumbered so
-    // that each XCD runs a contiguous range of tiles; either way the tiles
-    // are visited in groups of GROUP_M tile rows that share operand blocks.
-    const int G = A.tiles_m * A.tiles_n;
-    const int wg = blockIdx.x;
-    int pid = wg;
-    if (A.xcd_ranges) {
-        const int xcd = wg % NXCD, loc = wg / NXCD;
-        const int q = G / NXCD, rem = G % NXCD;
-        pid = xcd < rem ? xcd * (q + 1) + loc : rem * (q + 1) + (xcd - rem) * q + loc;
-    }
-    const int in_group = GROUP_M * A.tiles_n;
-    const int first_m = (pid / in_group) * GROUP_M;
-    const int gsz = min(A.tiles_m - first_m, GROUP_M);
-    const int tm = first_m + (pid % in_group) % gsz;
-    const int tn = (pid % in_group) / gsz;
-    const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
-
-    const int tid = threadIdx.x;
-    const int w = __builtin_amdgcn_readfirstlane(tid >> 6); // wave-uniform
-    const int l = tid & 63;
-    const int g = l >> 4, qd = l & 15; // lane group (K block / output row quad), row in fragment
-    const int wm = (w & 1) * WTM, wn = (w >> 1) * WTN;
-
-    v4f acc[FN][FM];
+    if constexpr (ELEM == MX_ELEM_E2M1) {
+        // two passes over the 32 tiles, first the low halves of the
+        // fragments (blocks 0-3 of the step), then the high halves: an
+        // accumulator's two instructions per step sit 32 apart instead of
+        // back to back, in the same order
+        auto pass = [&](auto hc) {
+            constexpr int H = decltype(hc)::value;
+            Half hb[FN], ha[FM];
+            hb[0] = read_half<0, H>(st, bb);
+            hb[1] = read_half<1, H>(st, bb);
+            hb[2] = read_half<2, H>(st, bb);
+            hb[3] = read_half<3, H>(st, bb);
+            ha[0] = read_half<0, H>(st, ba);
+            ha[1] = read_half<1, H>(st, ba);
+            auto column = [&](auto jc) {
+                constexpr int j = decltype(jc)::value;
+                if constexpr (j + 2 < FM)
+                    ha[j + 2] = read_half<j + 2, H>(st, ba);
+                __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int i = 0; i < FN; ++i)
-#pragma unroll
-        for (int j = 0; j < FM; ++j)
-            acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
-
-    LDS_AS uint8_t *st0 = (LDS_AS uint8_t *)lds;
-    const uint32_t st0_addr = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)st0);
-    const uint8_t *ta = A.a + m0 * A.rb, *tb = A.b + n0 * A.rb;
-    const uint8_t *tsa = A.as + m0 * A.rs, *tsb = A.bs + n0 * A.rs;
-    const Rows<ELEM> R = lane_rows<ELEM>(A, m0, n0, w, l);
-    const FragBase ba = frag_base<ELEM>(0, (BM + BN) * KB, wm, qd, g);
-    const FragBase bb = frag_base<ELEM>(BM * KB, (BM + BN) * KB + BM * SB, wn, qd, g);
-
-    // Pipeline, one barrier per K step.  At the top of step s every wave has
-    // its own DMA of step s landed (vmcnt) and, past the barrier, so has every
-    // other wave, and no wave still reads the other stage (step s-1): the DMA
-    // of step s+1 goes there.  The step then reads its four B fragments and
-    // streams the eight A fragments, each requested two ahead of the
-    // products that use it.
-    issue_step<ELEM>(ta, tb, tsa, tsb, R, 0, st0_addr, w);
-    for (int s = 0; s < A.steps; ++s) {
-        const int cur = s & 1;
-        wait_vmcnt0();
-        barrier();
-        if (s + 1 < A.steps)
-            issue_step<ELEM>(ta, tb, tsa, tsb, R, s + 1, st0_addr + (cur ^ 1) * STAGE, w);
-        const LDS_AS uint8_t *st = st0 + cur * STAGE;
-        Frag fb[FN], fa[FM];
-        fb[0] = read_frag<ELEM, 0>(st, bb);
-        fb[1] = read_frag<ELEM, 1>(st, bb);
-        fb[2] = read_frag<ELEM, 2>(st, bb);
-        fb[3] = read_frag<ELEM, 3>(st, bb);
-        fa[0] = read_frag<ELEM, 0>(st, ba);
-        fa[1] = read_frag<ELEM, 1>(st, ba);
-        auto column = [&](auto jc) {
-            constexpr int j = decltype(jc)::value;
-            if constexpr (j + 2 < FM)
-                fa[j + 2] = read_frag<ELEM, j + 2>(st, ba);
-            // keep the read ahead of this fragment's products
-            __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-            for (int i = 0; i < FN; ++i)
-                mma<ELEM>(acc[i][j], fb[i], fa[j]);
-            __builtin_amdgcn_sched_barrier(0);
+                for (int i = 0; i < FN; ++i)
+                    mma_half(acc[i][j], hb[i], ha[j]);
+                __builtin_amdgcn_sched_barrier(0);
+            };
+            column(std::integral_constant<int, 0>{});
+            column(std::integral_constant<int, 1>{});
+            column(std::integral_constant<int, 2>{});
+            column(std::integral_constant<int, 3>{});
+            column(std::integral_constant<int, 4>{});
+            column(std::integral_constant<int, 5>{});
+            column(std::integral_constant<int, 6>{});
+            column(std::integral_constant<int, 7>{});
         };
-        column(std::integral_constant<int, 0>{});
-        column(std::integral_constant<int, 1>{});
-        column(std::integral_constant<int, 2>{});
-        column(std::integral_constant<int, 3>{});
-        column(std::integral_constant<int, 4>{});
-        column(std::integral_constant<int, 5>{});
-        column(std::integral_constant<int, 6>{});
-        column(std::integral_constant<int, 7>{});
+        pass(std::integral_constant<int, 0>{});
+        pass(std::integral_constant<int, 1>{});
+        return;
     }
+    Frag fb[FN], fa[FM];
+    fb[0] = read_frag<ELEM, 0>(st, bb);
+    fb[1] = read_frag<ELEM, 1>(st, bb);
+    fb[2] = read_frag<ELEM, 2>(st, bb);
+    fb[3] = read_frag<ELEM, 3>(st, bb);
+    fa[0] = read_frag<ELEM, 0>(st, ba);
+    fa[1] = read_frag<ELEM, 1>(st, ba);
+    auto column = [&](auto jc) {
+        constexpr int j = decltype(jc)::value;
+        if constexpr (j + 2 < FM)
+            fa[j + 2] = read_frag<ELEM, j + 2>(st, ba);
+        // keep the read ahead of this fragment's products
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int i = 0; i < FN; ++i)
+            mma<ELEM>(acc[i][j], fb[i], fa[j]);
+        __builtin_amdgcn_sched_barrier(0);
+    };
+    column(std::integral_constant<int, 0>{});
+    column(std::integral_constant<int, 1>{});
+    column(std::integral_constant<int, 2>{});
+    column(std::integral_constant<int, 3>{});
+    column(std::integral_constant<int, 4>{});
+    column(std::integral_constant<int, 5>{});
+    column(std::integral_constant<int, 6>{});
+    column(std::integral_constant<int, 7>{});
+}
 
+// Store the workgroup's accumulators as H[m0 .., n0 ..] (f32 or bf16), times
+// the column gain if there is one.
+template <int OUT>
+__device__ __forceinline__ void store_tile(const Args &A, const v4f (&acc)[FN][FM], int64_t m0,
+                                           int64_t n0, int wm, int wn, int g, int qd)
+{
     // lane (g, qd) of tile (i, j) holds H[m][n .. n+3] with
     // m = m0 + wm + 16 j + qd and n = n0 + wn + 16 i + 4 g.  N is a multiple
     // of 16, so a tile column base below N has its 16 columns inside H.
@@ -400,10 +416,97 @@ __global__ void __launch_bounds__(NT) mx_gemm_kernel(Args A)
 }
 
 template <int ELEM, int OUT>
+__global__ void __launch_bounds__(NT) mx_gemm_kernel(Args A)
+{
+    constexpr int SB = Op<ELEM>::SB;
+    constexpr int STAGE = Op<ELEM>::STAGE;
+    __shared__ __attribute__((aligned(16))) uint8_t lds[2 * STAGE];
+
+    // Tiles.  The grid is at most one workgroup per compute unit, and
+    // workgroup b takes tiles v = b, b + grid, b + 2 grid, ...  Dispatch is
+    // round robin over the XCDs (each with its own L2).  With xcd_ranges, v
+    // is renumbered so that each XCD runs a contiguous range of tiles; either
+    // way the tiles are visited in groups of GROUP_M tile rows that share
+    // operand blocks.
+    const int G = A.tiles_m * A.tiles_n;
+    auto tile_of = [&](int v, int64_t &m0, int64_t &n0) {
+        int pid = v;
+        if (A.xcd_ranges) {
+            const int xcd = v % NXCD, loc = v / NXCD;
+            const int q = G / NXCD, rem = G % NXCD;
+            pid = xcd < rem ? xcd * (q + 1) + loc : rem * (q + 1) + (xcd - rem) * q + loc;
+        }
+        const int in_group = GROUP_M * A.tiles_n;
+        const int first_m = (pid / in_group) * GROUP_M;
+        const int gsz = min(A.tiles_m - first_m, GROUP_M);
+        m0 = (int64_t)(first_m + (pid % in_group) % gsz) * BM;
+        n0 = (int64_t)((pid % in_group) / gsz) * BN;
+    };
+
+    const int tid = threadIdx.x;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6); // wave-uniform
+    const int l = tid & 63;
+    const int g = l >> 4, qd = l & 15; // lane group (K block / output row quad), row in fragment
+    const int wm = (w & 1) * WTM, wn = (w >> 1) * WTN;
+
+    LDS_AS uint8_t *st0 = (LDS_AS uint8_t *)lds;
+    const uint32_t st0_addr = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)st0);
+    const FragBase ba = frag_base<ELEM>(0, (BM + BN) * KB, wm, qd, g);
+    const FragBase bb = frag_base<ELEM>(BM * KB, (BM + BN) * KB + BM * SB, wn, qd, g);
+
+    int v = blockIdx.x;
+    int64_t m0, n0;
+    tile_of(v, m0, n0);
+    Rows<ELEM> R = lane_rows<ELEM>(A, m0, n0, w, l);
+
+    // Pipeline, one barrier per K step.  At the top of a step every wave has
+    // its own DMA of the step landed (vmcnt) and, past the barrier, so has
+    // every other wave, and no wave still reads the other stage (the previous
+    // step): the DMA of the next step goes there, and after a tile's last
+    // step the DMA of the next tile's first step, which then runs under that
+    // last step's products and the tile's stores.
+    issue_step<ELEM>(A.a + m0 * A.rb, A.b + n0 * A.rb, A.as + m0 * A.rs, A.bs + n0 * A.rs, R, 0,
+                     st0_addr, w);
+    for (int gs = 0;;) {
+        v4f acc[FN][FM];
+#pragma unroll
+        for (int i = 0; i < FN; ++i)
+#pragma unroll
+            for (int j = 0; j < FM; ++j)
+                acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
+        const int nv = v + (int)gridDim.x;
+        int64_t m1 = 0, n1 = 0;
+        for (int s = 0; s < A.steps; ++s, ++gs) {
+            const int cur = gs & 1;
+            wait_vmcnt0();
+            barrier();
+            const uint32_t nxt = st0_addr + (cur ^ 1) * STAGE;
+            if (s + 1 < A.steps) {
+                issue_step<ELEM>(A.a + m0 * A.rb, A.b + n0 * A.rb, A.as + m0 * A.rs,
+                                 A.bs + n0 * A.rs, R, s + 1, nxt, w);
+            } else if (nv < G) {
+                tile_of(nv, m1, n1);
+                R = lane_rows<ELEM>(A, m1, n1, w, l);
+                issue_step<ELEM>(A.a + m1 * A.rb, A.b + n1 * A.rb, A.as + m1 * A.rs,
+                                 A.bs + n1 * A.rs, R, 0, nxt, w);
+            }
+            step_products<ELEM>(acc, st0 + cur * STAGE, ba, bb);
+        }
+        store_tile<OUT>(A, acc, m0, n0, wm, wn, g, qd);
+        if (nv >= G)
+            break;
+        v = nv;
+        m0 = m1;
+        n0 = n1;
+    }
+}
+
+template <int ELEM, int OUT>
 hipError_t launch(const Args &A, hipStream_t stream)
 {
     const int G = A.tiles_m * A.tiles_n;
-    hipLaunchKernelGGL((mx_gemm_kernel<ELEM, OUT>), dim3((unsigned)G), dim3(NT), 0, stream, A);
+    const int grid = G < A.grid_max ? G : A.grid_max;
+    hipLaunchKernelGGL((mx_gemm_kernel<ELEM, OUT>), dim3((unsigned)grid), dim3(NT), 0, stream, A);
     return hipGetLastError();
 }
 
@@ -414,6 +517,32 @@ hipError_t launch(const Args &A, hipStream_t stream)
 namespace {
 
 bool aligned(const void *p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
+
+// Compute units of the device `stream` runs on (the current device for the
+// null stream), looked up once per device; 0 if unknown.
+int compute_units(void *stream)
+{
+    static std::atomic<int> cache[64];
+    int dev = -1;
+    if (stream) {
+        hipDevice_t hd;
+        if (hipStreamGetDevice(static_cast<hipStream_t>(stream), &hd) != hipSuccess)
+            return 0;
+        dev = (int)hd;
+    } else if (hipGetDevice(&dev) != hipSuccess) {
+        return 0;
+    }
+    if (dev < 0 || dev >= 64)
+        return 0;
+    int n = cache[dev].load(std::memory_order_relaxed);
+    if (n == 0) {
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            n <= 0)
+            return 0;
+        cache[dev].store(n, std::memory_order_relaxed);
+    }
+    return n;
+}
 
 } // namespace
 
@@ -470,6 +599,10 @@ mx_status mx_matmul_fwd(const uint8_t *a_codes, const uint8_t *a_scales, const u
     // round robin from N = 16384 on (the gate+up shape, N = 28672: 1765 vs
     // 1842 us at M = 16384, and likewise at M = 4096 .. 32768).
     A.xcd_ranges = tn < 64 ? 1 : 0;
+    // one workgroup per compute unit (each holds 135-139 KB of LDS); with the
+    // count unknown, one workgroup per tile
+    const int cus = compute_units(stream);
+    A.grid_max = cus > 0 ? cus : (int)(tm * tn);
     hipStream_t st = static_cast<hipStream_t>(stream);
     hipError_t e;
     if (elem == MX_ELEM_E4M3)
