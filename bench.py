@@ -646,12 +646,18 @@ def main():
         n_sets, 60, 30, stream)
     ms_ct = time_launches(lambda i: mxnorm.mx_cast_t_fwd(xs[i], rho[i], codes=tc[i], scales=ts[i]),
                           n_sets, 60, 30, stream)
+    # the STE's traffic with no arithmetic: x and grad_Z read, grad_X written
+    ms_ste_ref = time_launches(lambda i: streamref.stream_reference_ste(xs[i], gzs[i], gxo[i]),
+                               n_sets, 60, 30, stream)
+    ste_ref_gbps = 3 * T * d * 2 / (ms_ste_ref * 1e-3) / 1e9
     bwd = {"ste_bwd": {"us": round(ms_ste * 1e3, 2),
                        "GB/s": round(ste_bytes(T, d) / (ms_ste * 1e-3) / 1e9, 1)},
            "cast_t_rho_x_mxfp8": {"us": round(ms_ct * 1e3, 2),
                                   "GB/s": round(cast_t_bytes(T, d) / (ms_ct * 1e-3) / 1e9, 1)}}
     for v in bwd.values():
         v["pct_of_peak"] = round(100 * v["GB/s"] / PEAK_HBM_GBPS, 2)
+    bwd["ste_bwd"]["stream_reference_GBps"] = round(ste_ref_gbps, 1)
+    bwd["ste_bwd"]["frac_of_stream_reference"] = round(bwd["ste_bwd"]["GB/s"] / ste_ref_gbps, 4)
     del gzs, gxo, wsp, tc, ts
 
     # the MX matmul the MXNorm output feeds (Llama-3-8B QKV projection)

@@ -239,8 +239,8 @@ mx_status mx_cast_t_fwd(const void *x, const float *rho, int64_t R, int64_t C, i
  * the forward returned.  grad_x: [T, d] float32 or bf16 (out_dtype).
  * Arithmetic: dXb exact in float, u summed in double, c = rho^3 u / d in
  * double rounded to float, grad_x = RN(RN(rho dXb) - RN(c x)); the
- * grad_gamma partial sums are float over at most 32 rows, then summed in
- * double in a fixed order (deterministic for a given T).  grad_gamma: float [d] or NULL (not computed);
+ * grad_gamma partial sums are float over the rows of one workgroup (at most
+ * 64), then summed in double in a fixed order (deterministic for a given T).  grad_gamma: float [d] or NULL (not computed);
  * it needs `workspace`, caller-owned device memory of at least
  * mxnorm_ste_bwd_workspace_bytes(T, d) bytes (16-byte aligned), overwritten.
  * d a multiple of 8 and <= MXNORM_MAX_D; 16-byte alignment of x, grad_z,
@@ -261,7 +261,7 @@ mx_status mxnorm_ste_bwd(const void *x, const void *grad_z, const void *gamma, c
  * hipMalloc, hipFree or allocating library routine.  Returns MX_EUNSUPPORTED,
  * before any launch, when grad_gamma is requested and
  * mxnorm_ste_bwd_workspace_bytes(T, d) exceeds that size (for example
- * T = 32768 fits up to d = 14336).  The device is the stream's (the current
+ * T = 32768 fits up to d = 16384).  The device is the stream's (the current
  * device for the null stream); its array's address is looked up on the first
  * call on that device.  All calls on one GPU share its array: calls that
  * overlap in time on one GPU (on different streams, or from several host

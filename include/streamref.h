@@ -39,6 +39,15 @@ extern "C" {
 int mx_stream_reference(const void *x, int64_t T, int64_t d, uint8_t *out, uint8_t *out_small,
                         int mode, void *stream);
 
+/*
+ * mx_stream_reference_ste moves the bytes of mxnorm_ste_bwd with bf16
+ * output: it reads x and grad_z, bf16 [T, d] each, and writes out, bf16
+ * [T, d] (their bitwise xor), one row per wave with 16-byte accesses.  Same
+ * size and alignment rules and return codes as mx_stream_reference.
+ */
+int mx_stream_reference_ste(const void *x, const void *grad_z, int64_t T, int64_t d, void *out,
+                            void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -531,50 +531,44 @@ ste_bwd_kernel(SteArgs A)
     }
 }
 
-// grad_gamma[j] = sum of the P partial rows, in double, in a fixed order, in
-// two launches so that the first one spreads over the whole chip:
-//  * slice pass: block (b, s) sums columns [64 b, 64 b + 64) over partial
-//    rows [s Ps, (s + 1) Ps) (Ps = ceil(P / GG_SLICES)); thread (g, c) adds
-//    rows s Ps + g, + 4, + 8, ... of column c in order, the 4 sums are added
-//    in order of g and stored as the double slice[s][j];
-//  * final pass: grad_gamma[j] = RN(sum over s of slice[s][j], in order).
-// Deterministic; each wave reads 256 contiguous bytes per partial row.
-constexpr int GG_SLICES = 16;
-constexpr int GG_GROUPS = 4;
-__global__ void __launch_bounds__(256) ggamma_slice_kernel(const float *part, int64_t P, int d,
-                                                           double *slice)
+// grad_gamma[j] = RN(sum of the P partial rows, in double, in a fixed
+// order), in one launch.  Block b (1024 threads) sums columns [64 b, +64):
+// thread (g, q), g = 0 .. 63, q = 0 .. 15, adds rows g, g + 64, g + 128, ...
+// of columns 64 b + 4 q .. +3 in order, 16 bytes per row, so every thread has
+// several loads in flight; the 64 row groups' sums are then added in order
+// of g.  Deterministic for a given P.  (Two launches, slices of rows then a
+// sum of the slices, took about 10 us at [32768, 4096]; 256 threads with
+// 4-byte loads per column were latency-bound.)
+constexpr int GG_GROUPS = 64;
+__global__ void __launch_bounds__(1024) ggamma_reduce_kernel(const float *part, int64_t P, int d,
+                                                             float *out)
 {
     __shared__ double red[GG_GROUPS][64];
-    const int c = threadIdx.x & 63, g = threadIdx.x >> 6;
-    const int j = blockIdx.x * 64 + c;
-    const int64_t Ps = (P + GG_SLICES - 1) / GG_SLICES;
-    const int64_t p0 = (int64_t)blockIdx.y * Ps, p1 = min(P, p0 + Ps);
-    double s = 0.0;
-    if (j < d)
+    const int q = threadIdx.x & 15, g = threadIdx.x >> 4;
+    const int j0 = blockIdx.x * 64 + 4 * q; // d % 8 == 0: j0 < d means j0 + 3 < d
+    double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+    if (j0 < d) {
 #pragma unroll 4
-        for (int64_t p = p0 + g; p < p1; p += GG_GROUPS)
-            s += (double)part[p * d + j];
-    red[g][c] = s;
+        for (int64_t p = g; p < P; p += GG_GROUPS) {
+            const float4 v = *reinterpret_cast<const float4 *>(part + p * d + j0);
+            s0 += (double)v.x;
+            s1 += (double)v.y;
+            s2 += (double)v.z;
+            s3 += (double)v.w;
+        }
+    }
+    red[g][4 * q] = s0;
+    red[g][4 * q + 1] = s1;
+    red[g][4 * q + 2] = s2;
+    red[g][4 * q + 3] = s3;
     lds_barrier();
-    if (g == 0 && j < d) {
+    const int c = threadIdx.x;
+    if (c < 64 && blockIdx.x * 64 + c < d) {
         double t = 0.0;
-#pragma unroll
         for (int i = 0; i < GG_GROUPS; ++i)
             t += red[i][c];
-        slice[(int64_t)blockIdx.y * d + j] = t;
+        out[blockIdx.x * 64 + c] = (float)t;
     }
-}
-
-__global__ void __launch_bounds__(256) ggamma_final_kernel(const double *slice, int d, float *out)
-{
-    const int j = blockIdx.x * 256 + threadIdx.x;
-    if (j >= d)
-        return;
-    double t = 0.0;
-#pragma unroll
-    for (int s = 0; s < GG_SLICES; ++s)
-        t += slice[(int64_t)s * d + j];
-    out[j] = (float)t;
 }
 
 template <int NT, int CPL, int OUT, bool GAM>
@@ -728,9 +722,8 @@ size_t mxnorm_ste_bwd_workspace_bytes(int64_t T, int64_t d)
 {
     if (T <= 0 || d <= 0)
         return 0;
-    // the workgroups' partial rows (float), then the reduction's slices (double)
-    return (size_t)ste_workgroups(T) * (size_t)d * sizeof(float) +
-           (size_t)mxb::GG_SLICES * (size_t)d * sizeof(double);
+    // one float partial row of grad_gamma per workgroup
+    return (size_t)ste_workgroups(T) * (size_t)d * sizeof(float);
 }
 
 mx_status mxnorm_ste_bwd(const void *x, const void *grad_z, const void *gamma, const float *rho,
@@ -785,19 +778,10 @@ mx_status mxnorm_ste_bwd(const void *x, const void *grad_z, const void *gamma, c
         e = gamma ? mxb::launch_ste_out<MX_OUT_BF16, true>(A, st)
                   : mxb::launch_ste_out<MX_OUT_BF16, false>(A, st);
     if (e == hipSuccess && grad_gamma) {
-        const int64_t P = ste_workgroups(T);
-        // P d floats keep the slices 8-byte aligned (d % 8 == 0)
-        double *slice = reinterpret_cast<double *>(static_cast<float *>(workspace) + P * d);
-        hipLaunchKernelGGL(mxb::ggamma_slice_kernel,
-                           dim3((unsigned)((d + 63) / 64), (unsigned)mxb::GG_SLICES), dim3(256), 0,
-                           st, static_cast<const float *>(workspace), P, (int)d, slice);
+        hipLaunchKernelGGL(mxb::ggamma_reduce_kernel, dim3((unsigned)((d + 63) / 64)), dim3(1024), 0,
+                           st, static_cast<const float *>(workspace), ste_workgroups(T), (int)d,
+                           grad_gamma);
         e = hipGetLastError();
-        if (e == hipSuccess) {
-            hipLaunchKernelGGL(mxb::ggamma_final_kernel, dim3((unsigned)((d + 255) / 256)),
-                               dim3(256), 0, st, static_cast<const double *>(slice), (int)d,
-                               grad_gamma);
-            e = hipGetLastError();
-        }
     }
     if (e != hipSuccess)
         return mxk::fail(MX_EHIP, "kernel launch failed: %s", hipGetErrorString(e));

@@ -92,7 +92,48 @@ __global__ void __launch_bounds__(256) stream_kernel(const uint4 *x, int64_t T, 
                                     reinterpret_cast<u32x4v *>(out_small + rr * K + 16 * lane));
 }
 
+// The straight-through estimator's traffic: per row, x and grad_z read and
+// grad_x written, bf16 [T, d] each, one row per wave, 16-byte accesses, all
+// loads of a row issued before its stores.
+__global__ void __launch_bounds__(256) ste_stream_kernel(const uint4 *x, const uint4 *gz, int64_t T,
+                                                         int nc, uint4 *out)
+{
+    const int lane = threadIdx.x & 63;
+    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= T)
+        return;
+    const int cpl = nc / 64;
+    uint4 a[8], b[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const int64_t c = row * nc + (j < cpl ? j * 64 : 0) + lane;
+        a[j] = load_stream(x + c);
+        b[j] = load_stream(gz + c);
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+        if (j < cpl)
+            out[row * nc + j * 64 + lane] =
+                make_uint4(a[j].x ^ b[j].x, a[j].y ^ b[j].y, a[j].z ^ b[j].z, a[j].w ^ b[j].w);
+}
+
 } // namespace
+
+extern "C" int mx_stream_reference_ste(const void *x, const void *grad_z, int64_t T, int64_t d,
+                                       void *out, void *stream)
+{
+    if (T < 0 || d <= 0 || d % 512 != 0 || d > 4096 || T > ((int64_t)1 << 34))
+        return 1;
+    if (T == 0)
+        return 0;
+    if (!x || !grad_z || !out || (uintptr_t)x % 16 || (uintptr_t)grad_z % 16 ||
+        (uintptr_t)out % 16)
+        return 1;
+    hipLaunchKernelGGL(ste_stream_kernel, dim3((unsigned)((T + 3) / 4)), dim3(256), 0,
+                       (hipStream_t)stream, static_cast<const uint4 *>(x),
+                       static_cast<const uint4 *>(grad_z), T, (int)(d / 8), static_cast<uint4 *>(out));
+    return hipGetLastError() == hipSuccess ? 0 : 3;
+}
 
 extern "C" int mx_stream_reference(const void *x, int64_t T, int64_t d, uint8_t *out,
                                    uint8_t *out_small, int mode, void *stream)

@@ -21,6 +21,9 @@ def load():
         lib.mx_stream_reference.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
                                             ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
                                             ctypes.c_void_p]
+        lib.mx_stream_reference_ste.restype = ctypes.c_int
+        lib.mx_stream_reference_ste.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                                ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]
         _lib = lib
     return _lib
 
@@ -36,3 +39,15 @@ def stream_reference(x, out, out_small, mode="mixed"):
                                     ctypes.c_void_p(torch.cuda.current_stream(x.device).cuda_stream))
     if st != 0:
         raise RuntimeError("mx_stream_reference failed with status %d" % st)
+
+
+def stream_reference_ste(x, grad_z, out):
+    """x, grad_z, out: bf16 [T, d] (d % 512 == 0, d <= 4096): the straight-
+    through estimator's traffic with no arithmetic."""
+    T, d = x.shape
+    st = load().mx_stream_reference_ste(ctypes.c_void_p(x.data_ptr()),
+                                        ctypes.c_void_p(grad_z.data_ptr()), T, d,
+                                        ctypes.c_void_p(out.data_ptr()),
+                                        ctypes.c_void_p(torch.cuda.current_stream(x.device).cuda_stream))
+    if st != 0:
+        raise RuntimeError("mx_stream_reference_ste failed with status %d" % st)

@@ -57,6 +57,16 @@ def test_stream_reference_rejects_bad_arguments():
     assert f(None, 0, 4096, None, None, 0, None) == 0       # T = 0: no-op
 
 
+def test_ste_stream_reference_rejects_bad_arguments():
+    from paper_2603_13180_amd import streamref
+    f = streamref.load().mx_stream_reference_ste
+    assert f(A16, A16, 4, 1000, OUT, None) == 1              # d % 512
+    assert f(A16, A16, 4, 8192, OUT, None) == 1              # d > 4096
+    assert f(A16, A8, 4, 4096, OUT, None) == 1               # alignment
+    assert f(A16, A16, -1, 4096, OUT, None) == 1
+    assert f(None, None, 0, 4096, None, None) == 0           # T = 0: no-op
+
+
 def test_header_compiles_as_c():
     import subprocess
     import tempfile
@@ -218,13 +228,12 @@ def test_mx_cast_t_rejects_bad_arguments(args, status):
 
 def test_ste_workspace_size():
     # one float partial row of grad_gamma per workgroup of rpw rows, rpw =
-    # clamp(ceil(T / 512), 4, 64), then 16 double rows of the reduction's slices
+    # clamp(ceil(T / 512), 4, 64)
     lib = mxnorm.load()
     assert lib.mxnorm_ste_bwd_workspace_bytes(0, 4096) == 0
     for T in (1, 4, 5, 32, 33, 2048, 4096, 4097, 32768, 100000):
         rpw = max(4, min(64, -(-T // 512)))
-        assert lib.mxnorm_ste_bwd_workspace_bytes(T, 4096) == \
-            -(-T // rpw) * 4096 * 4 + 16 * 4096 * 8, T
+        assert lib.mxnorm_ste_bwd_workspace_bytes(T, 4096) == -(-T // rpw) * 4096 * 4, T
 
 
 @pytest.mark.parametrize("args,status", [
@@ -248,8 +257,8 @@ def test_ste_noalloc_rejects_sizes_beyond_its_array():
     lib = mxnorm.load()
     cap = lib.mxnorm_ste_bwd_noalloc_max_workspace()
     assert cap == 32 << 20
-    assert lib.mxnorm_ste_bwd_workspace_bytes(32768, 14336) <= cap
-    for T, d in ((131072, 8192), (32768, 16384), (1 << 20, 4096)):
+    assert lib.mxnorm_ste_bwd_workspace_bytes(32768, 16384) <= cap
+    for T, d in ((131072, 8192), (32768, 32768), (1 << 20, 4096)):
         assert lib.mxnorm_ste_bwd_workspace_bytes(T, d) > cap
         assert lib.mxnorm_ste_bwd_noalloc(A16, A16, None, OUT, T, d, 1, OUT, OUT, None) == 2
         assert b"allocation-free" in lib.mx_last_error()
