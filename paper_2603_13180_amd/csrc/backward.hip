@@ -38,11 +38,18 @@ using namespace mxk;
 // ---------------------------------------------------------- column cast --
 
 constexpr int CT_ROWS = 128;  // tile rows (four 32-row blocks)
-constexpr int CT_COLS = 128;  // tile columns (64 per pass of the 256 threads)
-constexpr int CT_TILES = 16;  // most tiles per workgroup (a span of up to 2048 rows)
-constexpr int CT_CPR = CT_COLS / 8;       // 16-byte chunks per tile row
-constexpr int CT_RPP = 256 / CT_CPR;      // tile rows per staging pass
-constexpr int CT_NLD = CT_ROWS / CT_RPP;  // staging loads per thread
+
+// Tile shapes: COLS tile columns (64 per pass of the 256 threads), at most
+// TILES tiles per workgroup.
+template <int COLS> struct CtShape {
+    static constexpr int TILES = COLS == 256 ? 8 : 16;
+    static constexpr int CPR = COLS / 8;          // 16-byte chunks per tile row
+    static constexpr int RPP = 256 / CPR;         // tile rows per staging pass
+    static constexpr int NLD = CT_ROWS / RPP;     // staging loads per thread
+    static constexpr int PITCH = COLS * 2;        // bytes per staged row
+    static constexpr int BLKB = 32 * PITCH + 32;  // bytes per staged 32-row block
+    static __device__ __forceinline__ int off(int r) { return (r >> 5) * BLKB + (r & 31) * PITCH; }
+};
 
 struct CastTArgs {
     const uint16_t *x;
@@ -51,17 +58,19 @@ struct CastTArgs {
     uint8_t *scales;
     int64_t R, C;
     int mode;
-    int tiles; // tiles per span, 1 .. CT_TILES
+    int tiles; // tiles per span, 1 .. CtShape<COLS>::TILES
 };
 
-// Workgroup (span, tile_c) casts columns [128 tile_c, +128) over a span of
+// Workgroup (span, tile_c) casts columns [COLS tile_c, +COLS) over a span of
 // `tiles` x 128 rows, 128 rows at a time (the host sizes the span so that
-// the grid still fills the chip).  Each 128 x 128 tile is staged in LDS as
-// it is in x (256 bytes per row, 32 bytes of padding after every 32 rows;
-// the next tile's loads are already in flight in registers).  The 256-byte
-// row pieces read from x are what sets the tile width: a transposing stream
-// with 128-byte pieces runs ~12% slower.  The tile is cast in two passes of
-// 64 columns; in pass h wave w casts columns 64h + 16w .. +15: lane 4 cc + b
+// the grid still fills the chip).  Each 128 x COLS tile is staged in LDS as
+// it is in x (2 COLS bytes per row, 32 bytes of padding after every 32 rows;
+// the next tile's loads are already in flight in registers).  The row pieces
+// read from x are what sets the tile width: a transposing stream with
+// 128-byte pieces runs ~12% slower than with 256; 512-byte pieces (COLS =
+// 256) make the cast of a wide matrix (C = 28672) 9% faster, and that of
+// C = 4096 3% slower.  The tile is cast in COLS / 64 passes of 64 columns;
+// in pass h wave w casts columns 64h + 16w .. +15: lane 4 cc + b
 // takes column 64h + 16w + cc over rows 32b .. 32b+31 (one scale block),
 // reads its 32 values down the column, scales them by rho, decides the E8M0
 // byte from their absmax and writes 32 codes (E4M3: 32 B; E2M1: 16 B) into
@@ -72,13 +81,12 @@ struct CastTArgs {
 // apart).  The span's scale bytes per column are gathered in LDS and
 // written at the end, 64 contiguous bytes per output row, rather than one
 // scattered byte per tile.
-constexpr int CT_PITCH = CT_COLS * 2;           // bytes per staged row
-constexpr int CT_BLKB = 32 * CT_PITCH + 32;     // bytes per staged 32-row block
-__device__ __forceinline__ int ct_off(int r) { return (r >> 5) * CT_BLKB + (r & 31) * CT_PITCH; }
-
-template <bool FP4>
+template <bool FP4, int COLS>
 __global__ void __launch_bounds__(256) cast_t_kernel(CastTArgs A)
 {
+    using S = CtShape<COLS>;
+    constexpr int CT_COLS = COLS, CT_TILES = S::TILES, CT_CPR = S::CPR, CT_RPP = S::RPP,
+                  CT_NLD = S::NLD, CT_PITCH = S::PITCH, CT_BLKB = S::BLKB;
     __shared__ __attribute__((aligned(16))) uint8_t tile[4 * CT_BLKB];
     __shared__ __attribute__((aligned(16))) float rs[CT_ROWS];
     __shared__ __attribute__((aligned(16))) uint8_t sb[CT_COLS][CT_TILES * 4];
@@ -125,7 +133,7 @@ __global__ void __launch_bounds__(256) cast_t_kernel(CastTArgs A)
         const int64_t r0 = span0 + (int64_t)t * CT_ROWS;
 #pragma unroll
         for (int k = 0; k < CT_NLD; ++k)
-            *reinterpret_cast<uint4 *>(&tile[ct_off(rbase + CT_RPP * k) + 16 * ch]) = nxt[k];
+            *reinterpret_cast<uint4 *>(&tile[S::off(rbase + CT_RPP * k) + 16 * ch]) = nxt[k];
         if (tid < CT_ROWS)
             rs[tid] = nrho;
         lds_barrier();
@@ -697,21 +705,31 @@ mx_status mx_cast_t_fwd(const void *x, const float *rho, int64_t R, int64_t C, i
     A.R = R;
     A.C = C;
     A.mode = scale_mode;
+    // tile width: 256 columns from C = 8192 on, else 128 (see the kernel);
     // tiles per workgroup: as many as keep about 2048 workgroups (longer
-    // spans write longer runs of scale bytes), at most CT_TILES
-    const int64_t col_tiles = (C + mxb::CT_COLS - 1) / mxb::CT_COLS;
+    // spans write longer runs of scale bytes), at most the shape's TILES
+    const bool wide = C >= 8192;
+    const int cols = wide ? 256 : 128;
+    const int max_tiles = wide ? mxb::CtShape<256>::TILES : mxb::CtShape<128>::TILES;
+    const int64_t col_tiles = (C + cols - 1) / cols;
     const int64_t row_tiles = (R + mxb::CT_ROWS - 1) / mxb::CT_ROWS;
-    A.tiles = (int)std::max<int64_t>(1, std::min<int64_t>(mxb::CT_TILES,
-                                                          col_tiles * row_tiles / 2048));
+    A.tiles = (int)std::max<int64_t>(1, std::min<int64_t>(max_tiles, col_tiles * row_tiles / 2048));
     const int64_t span = (int64_t)mxb::CT_ROWS * A.tiles;
     const dim3 grid((unsigned)col_tiles, (unsigned)((R + span - 1) / span));
     if (grid.y > 65535u)
         return mxk::fail(MX_EUNSUPPORTED, "R too large for one launch");
     hipStream_t st = static_cast<hipStream_t>(stream);
-    if (elem == MX_ELEM_E4M3)
-        hipLaunchKernelGGL(mxb::cast_t_kernel<false>, grid, dim3(256), 0, st, A);
-    else
-        hipLaunchKernelGGL(mxb::cast_t_kernel<true>, grid, dim3(256), 0, st, A);
+    if (elem == MX_ELEM_E4M3) {
+        if (wide)
+            hipLaunchKernelGGL((mxb::cast_t_kernel<false, 256>), grid, dim3(256), 0, st, A);
+        else
+            hipLaunchKernelGGL((mxb::cast_t_kernel<false, 128>), grid, dim3(256), 0, st, A);
+    } else {
+        if (wide)
+            hipLaunchKernelGGL((mxb::cast_t_kernel<true, 256>), grid, dim3(256), 0, st, A);
+        else
+            hipLaunchKernelGGL((mxb::cast_t_kernel<true, 128>), grid, dim3(256), 0, st, A);
+    }
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess)
         return mxk::fail(MX_EHIP, "kernel launch failed: %s", hipGetErrorString(e));
