@@ -49,6 +49,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <hip/hip_runtime_api.h> /* hipStream_t (host C code: -D__HIP_PLATFORM_AMD__) */
+
 #ifdef __cplusplus
 extern "C" {
 #endif
@@ -90,7 +92,7 @@ typedef enum {
  */
 mx_status mxnorm_mxfp8_fwd(const void *x, int64_t T, int64_t d, int p, float coef, float eps,
                            int scale_mode, uint8_t *codes, uint8_t *scales, float *rho,
-                           void *stream);
+                           hipStream_t stream);
 
 /*
  * RMSNorm, optional gain, then the MXFP8 cast (Algorithm 1; Sec. 3.1 eq.
@@ -101,7 +103,7 @@ mx_status mxnorm_mxfp8_fwd(const void *x, int64_t T, int64_t d, int p, float coe
  */
 mx_status rmsnorm_mxfp8_fwd(const void *x, const void *gamma, int64_t T, int64_t d, float eps,
                             int scale_mode, uint8_t *codes, uint8_t *scales, float *rho,
-                            void *stream);
+                            hipStream_t stream);
 
 /*
  * MXNorm with NVFP4 output: 16-element blocks, E4M3 block scales, a float
@@ -116,12 +118,12 @@ mx_status rmsnorm_mxfp8_fwd(const void *x, const void *gamma, int64_t T, int64_t
  */
 mx_status mxnorm_nvfp4_fwd(const void *x, int64_t T, int64_t d, int p, float coef, float eps,
                            float global_scale, uint8_t *codes, uint8_t *scales, float *rho,
-                           void *stream);
+                           hipStream_t stream);
 
 /* RMSNorm (+ optional gain) then the NVFP4 cast, as above with y for t. */
 mx_status rmsnorm_nvfp4_fwd(const void *x, const void *gamma, int64_t T, int64_t d, float eps,
                             float global_scale, uint8_t *codes, uint8_t *scales, float *rho,
-                            void *stream);
+                            hipStream_t stream);
 
 /*
  * MXNorm with a general MX output: `block` in {16, 32, 64} elements per E8M0
@@ -135,7 +137,7 @@ mx_status rmsnorm_nvfp4_fwd(const void *x, const void *gamma, int64_t T, int64_t
  */
 mx_status mxnorm_mx_fwd(const void *x, int64_t T, int64_t d, int block, int elem, int p,
                         float coef, float eps, int scale_mode, uint8_t *codes, uint8_t *scales,
-                        float *rho, void *stream);
+                        float *rho, hipStream_t stream);
 
 /*
  * Post-round MXNorm (the post-round appendix; an ablation the paper reports
@@ -154,7 +156,7 @@ mx_status mxnorm_mx_fwd(const void *x, int64_t T, int64_t d, int block, int elem
  */
 mx_status mxnorm_postround_mx_fwd(const void *x, int64_t T, int64_t d, int block, int elem,
                                   float eps, int scale_mode, uint8_t *codes, uint8_t *scales,
-                                  float *rho, void *stream);
+                                  float *rho, hipStream_t stream);
 
 /* The post-round table for `block` (16, 32, 64): x[i] = RN32(2^(i/64)),
  * v[i] = RN32(f^-1(x[i])), i = 0..64; host arrays of 65 floats. */
@@ -163,7 +165,7 @@ int mxnorm_postround_table(int block, float *x, float *v);
 /* RMSNorm (+ optional gain) then the general MX cast (Algorithm 1). */
 mx_status rmsnorm_mx_fwd(const void *x, const void *gamma, int64_t T, int64_t d, int block,
                          int elem, float eps, int scale_mode, uint8_t *codes, uint8_t *scales,
-                         float *rho, void *stream);
+                         float *rho, hipStream_t stream);
 
 /*
  * The plain MX cast of x, or of x * gamma (gamma NULL or bf16 [d]), with no
@@ -175,7 +177,7 @@ mx_status rmsnorm_mx_fwd(const void *x, const void *gamma, int64_t T, int64_t d,
  * (mx-matmul); the implementation appendix's mx_norm_linear_forward).
  */
 mx_status mx_cast_fwd(const void *x, const void *gamma, int64_t T, int64_t d, int block,
-                      int elem, int scale_mode, uint8_t *codes, uint8_t *scales, void *stream);
+                      int elem, int scale_mode, uint8_t *codes, uint8_t *scales, hipStream_t stream);
 
 typedef enum {
     MX_OUT_F32 = 0,       /* float32 output */
@@ -205,7 +207,7 @@ typedef enum {
  */
 mx_status mx_matmul_fwd(const uint8_t *a_codes, const uint8_t *a_scales, const uint8_t *b_codes,
                         const uint8_t *b_scales, int64_t M, int64_t N, int64_t K, int block,
-                        int elem, const void *b_gain, int out_dtype, void *out, void *stream);
+                        int elem, const void *b_gain, int out_dtype, void *out, hipStream_t stream);
 /* b_gain: bf16 [N] or NULL.  When given, H[m][n] = RN(acc * b_gain[n]) in
  * float: the gain applied after the product, as the weight gradient needs
  * (Sec. 3.7: grad W = MXCast(grad_H^T) MXCast(rho~ . X) . gamma); 8-byte
@@ -225,7 +227,7 @@ mx_status mx_matmul_fwd(const uint8_t *a_codes, const uint8_t *a_scales, const u
  * codes 16-byte aligned, rho 4-byte.  R == 0 is a no-op.
  */
 mx_status mx_cast_t_fwd(const void *x, const float *rho, int64_t R, int64_t C, int block,
-                        int elem, int scale_mode, uint8_t *codes, uint8_t *scales, void *stream);
+                        int elem, int scale_mode, uint8_t *codes, uint8_t *scales, hipStream_t stream);
 
 /*
  * The straight-through estimator of the MXNorm backward (Sec. 3.7: RMSNorm's
@@ -249,7 +251,7 @@ mx_status mx_cast_t_fwd(const void *x, const float *rho, int64_t R, int64_t C, i
 size_t mxnorm_ste_bwd_workspace_bytes(int64_t T, int64_t d);
 mx_status mxnorm_ste_bwd(const void *x, const void *grad_z, const void *gamma, const float *rho,
                          int64_t T, int64_t d, int out_dtype, void *grad_x, float *grad_gamma,
-                         void *workspace, size_t workspace_bytes, void *stream);
+                         void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
  * mxnorm_ste_bwd without a workspace argument, for callers that cannot
@@ -271,7 +273,7 @@ mx_status mxnorm_ste_bwd(const void *x, const void *grad_z, const void *gamma, c
 size_t mxnorm_ste_bwd_noalloc_max_workspace(void);
 mx_status mxnorm_ste_bwd_noalloc(const void *x, const void *grad_z, const void *gamma,
                                  const float *rho, int64_t T, int64_t d, int out_dtype,
-                                 void *grad_x, float *grad_gamma, void *stream);
+                                 void *grad_x, float *grad_gamma, hipStream_t stream);
 
 /*
  * Default NVFP4 tensor decode scales: an output bound divided by 6 * 448, so

@@ -27,6 +27,8 @@
 
 #include <stdint.h>
 
+#include <hip/hip_runtime_api.h> /* hipStream_t (host C code: -D__HIP_PLATFORM_AMD__) */
+
 #ifdef __cplusplus
 extern "C" {
 #endif
@@ -37,7 +39,7 @@ extern "C" {
 #define MX_STREAM_NVFP4 3
 
 int mx_stream_reference(const void *x, int64_t T, int64_t d, uint8_t *out, uint8_t *out_small,
-                        int mode, void *stream);
+                        int mode, hipStream_t stream);
 
 /*
  * mx_stream_reference_ste moves the bytes of mxnorm_ste_bwd with bf16
@@ -46,7 +48,7 @@ int mx_stream_reference(const void *x, int64_t T, int64_t d, uint8_t *out, uint8
  * size and alignment rules and return codes as mx_stream_reference.
  */
 int mx_stream_reference_ste(const void *x, const void *grad_z, int64_t T, int64_t d, void *out,
-                            void *stream);
+                            hipStream_t stream);
 
 #ifdef __cplusplus
 }

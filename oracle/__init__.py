@@ -75,6 +75,7 @@ def _load():
         "mxo_scale_exponent_fmt_array": (None, [P, I64, I, I, P]),
         "mxo_mxcast": (None, [P, I64, I64, I, I, I, P, P]),
         "mxo_mxnorm_mx": (None, [P, I64, I64, I, I, I, F, F, I, P, P, P, P]),
+        "mxo_cast_given_rho": (None, [P, P, I64, I64, I, I, I, P, P]),
         "mxo_rmsnorm_mx": (None, [P, P, I64, I64, I, I, F, I, P, P, P, P]),
         "mxo_mxcast_gain": (None, [P, P, I64, I64, I, I, I, P, P]),
         "mxo_mxcast_t": (ctypes.c_int, [P, P, I64, I64, I, I, I, P, P]),
@@ -292,6 +293,23 @@ def mxnorm_mx(x, B=32, elem="e4m3", p=2, coef_=None, eps=1e-6, mode="rceil"):
     _load().mxo_mxnorm_mx(_ptr(x), T, d, B, ELEMS[elem], p, c, eps, SCALE_MODES[mode],
                           _ptr(codes), _ptr(scales), _ptr(r32), _ptr(r64))
     return codes, scales, r32, r64
+
+
+def cast_given_rho(x, rho32, B=32, elem="e4m3", mode="rceil"):
+    """Algorithm 2's cast stage for a given float32 rho per row: scale bytes
+    and codes of t = RN32(x rho) (the second part of the two-part contract).
+    Returns (codes, scales)."""
+    x = _as_bf16_rows(x)
+    T, d = x.shape
+    rho32 = np.ascontiguousarray(rho32, dtype=np.float32)
+    if rho32.shape != (T,):
+        raise ValueError("rho32 must be float32 [T]")
+    cshape, sshape = _mx_shapes(T, d, B, elem)
+    codes = np.empty(cshape, np.uint8)
+    scales = np.empty(sshape, np.uint8)
+    _load().mxo_cast_given_rho(_ptr(x), _ptr(rho32), T, d, B, ELEMS[elem], SCALE_MODES[mode],
+                               _ptr(codes), _ptr(scales))
+    return codes, scales
 
 
 def rmsnorm_mx(x, gamma=None, B=32, elem="e4m3", eps=1e-6, mode="rceil"):

@@ -437,6 +437,31 @@ void mxo_mxnorm_mx(const uint16_t *x, int64_t T, int64_t d, int B, int elem, int
     }
 }
 
+/* Steps 3-4 of Algorithm 2 for a given per-row rho (rho [T], float): the
+ * cast stage on its own.  Whatever rho a kernel computed, its scale bytes and
+ * codes must follow from that rho this way (the second part of the two-part
+ * contract of the reading of R7).  t = RN32(x rho), then the plain MX cast of
+ * every block of t (eq. (blockscale), eq. (blockvals)); block k's scale comes
+ * from max|t| = RN32(m~_k rho) by monotonicity, and NaN blocks take their
+ * codes' signs from x (R8), as in mxo_mxnorm_mx. */
+void mxo_cast_given_rho(const uint16_t *x, const float *rho, int64_t T, int64_t d, int B,
+                        int elem, int mode, uint8_t *codes, uint8_t *scales)
+{
+    int64_t K = d / B, t, k;
+    float y[64];
+    uint8_t rowcodes[65536];
+    for (t = 0; t < T; t++) {
+        const uint16_t *xr = x + t * d;
+        for (k = 0; k < K; k++) {
+            int b;
+            for (b = 0; b < B; b++)
+                y[b] = mxo_bf16_to_float(xr[k * B + b]) * rho[t]; /* RN32(x rho) */
+            scales[t * K + k] = mx_cast_block(y, xr + k * B, B, mode, elem, rowcodes + k * B);
+        }
+        store_row_codes(rowcodes, d, elem, codes + t * (elem == MXO_ELEM_E2M1 ? d / 2 : d));
+    }
+}
+
 /* MXFP8: 32-element blocks, E4M3 elements. */
 void mxo_mxnorm_mxfp8(const uint16_t *x, int64_t T, int64_t d, int p, float coef, float eps,
                       int mode, uint8_t *codes, uint8_t *scales, float *rho32, double *rho64)

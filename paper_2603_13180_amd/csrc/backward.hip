@@ -633,7 +633,7 @@ void *scratch_ptr[kMaxDevices];
 
 // The scratch address on the device that `stream` belongs to (the current
 // device for the null stream), or an error.
-mx_status scratch_for(void *stream, void **out)
+mx_status scratch_for(hipStream_t stream, void **out)
 {
     int dev = -1;
     hipError_t e;
@@ -674,7 +674,7 @@ mx_status scratch_for(void *stream, void **out)
 extern "C" {
 
 mx_status mx_cast_t_fwd(const void *x, const float *rho, int64_t R, int64_t C, int block,
-                        int elem, int scale_mode, uint8_t *codes, uint8_t *scales, void *stream)
+                        int elem, int scale_mode, uint8_t *codes, uint8_t *scales, hipStream_t stream)
 {
     mxk::clear_error();
     if (R < 0 || C <= 0)
@@ -746,7 +746,7 @@ size_t mxnorm_ste_bwd_workspace_bytes(int64_t T, int64_t d)
 
 mx_status mxnorm_ste_bwd(const void *x, const void *grad_z, const void *gamma, const float *rho,
                          int64_t T, int64_t d, int out_dtype, void *grad_x, float *grad_gamma,
-                         void *workspace, size_t workspace_bytes, void *stream)
+                         void *workspace, size_t workspace_bytes, hipStream_t stream)
 {
     mxk::clear_error();
     if (T < 0)
@@ -810,7 +810,7 @@ size_t mxnorm_ste_bwd_noalloc_max_workspace(void) { return kScratchBytes; }
 
 mx_status mxnorm_ste_bwd_noalloc(const void *x, const void *grad_z, const void *gamma,
                                  const float *rho, int64_t T, int64_t d, int out_dtype,
-                                 void *grad_x, float *grad_gamma, void *stream)
+                                 void *grad_x, float *grad_gamma, hipStream_t stream)
 {
     mxk::clear_error();
     if (grad_gamma && T > 0 && d > 0 && mxnorm_ste_bwd_workspace_bytes(T, d) > kScratchBytes)

@@ -520,7 +520,7 @@ bool aligned(const void *p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0;
 
 // Compute units of the device `stream` runs on (the current device for the
 // null stream), looked up once per device; 0 if unknown.
-int compute_units(void *stream)
+int compute_units(hipStream_t stream)
 {
     static std::atomic<int> cache[64];
     int dev = -1;
@@ -550,7 +550,7 @@ extern "C" {
 
 mx_status mx_matmul_fwd(const uint8_t *a_codes, const uint8_t *a_scales, const uint8_t *b_codes,
                         const uint8_t *b_scales, int64_t M, int64_t N, int64_t K, int block,
-                        int elem, const void *b_gain, int out_dtype, void *out, void *stream)
+                        int elem, const void *b_gain, int out_dtype, void *out, hipStream_t stream)
 {
     mxk::clear_error();
     if (M < 0 || N < 0 || K <= 0)

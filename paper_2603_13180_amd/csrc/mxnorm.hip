@@ -155,7 +155,7 @@ mx_status check_global_scale(float s_g)
     return MX_OK;
 }
 
-mx_status run(Args A, int fmt, int kind, void *stream)
+mx_status run(Args A, int fmt, int kind, hipStream_t stream)
 {
     int TL, CPL;
     pick_team(A.T, A.nc, TL, CPL);
@@ -334,7 +334,7 @@ extern "C" {
 
 mx_status mxnorm_mxfp8_fwd(const void *x, int64_t T, int64_t d, int p, float coef, float eps,
                            int scale_mode, uint8_t *codes, uint8_t *scales, float *rho,
-                           void *stream)
+                           hipStream_t stream)
 {
     clear_error();
     mx_status st = check_common(x, nullptr, T, d, 32, eps, codes, scales, rho);
@@ -351,7 +351,7 @@ mx_status mxnorm_mxfp8_fwd(const void *x, int64_t T, int64_t d, int p, float coe
 
 mx_status rmsnorm_mxfp8_fwd(const void *x, const void *gamma, int64_t T, int64_t d, float eps,
                             int scale_mode, uint8_t *codes, uint8_t *scales, float *rho,
-                            void *stream)
+                            hipStream_t stream)
 {
     clear_error();
     mx_status st = check_common(x, gamma, T, d, 32, eps, codes, scales, rho);
@@ -366,7 +366,7 @@ mx_status rmsnorm_mxfp8_fwd(const void *x, const void *gamma, int64_t T, int64_t
 
 mx_status mxnorm_nvfp4_fwd(const void *x, int64_t T, int64_t d, int p, float coef, float eps,
                            float global_scale, uint8_t *codes, uint8_t *scales, float *rho,
-                           void *stream)
+                           hipStream_t stream)
 {
     clear_error();
     mx_status st = check_common(x, nullptr, T, d, 16, eps, codes, scales, rho);
@@ -383,7 +383,7 @@ mx_status mxnorm_nvfp4_fwd(const void *x, int64_t T, int64_t d, int p, float coe
 
 mx_status rmsnorm_nvfp4_fwd(const void *x, const void *gamma, int64_t T, int64_t d, float eps,
                             float global_scale, uint8_t *codes, uint8_t *scales, float *rho,
-                            void *stream)
+                            hipStream_t stream)
 {
     clear_error();
     mx_status st = check_common(x, gamma, T, d, 16, eps, codes, scales, rho);
@@ -398,7 +398,7 @@ mx_status rmsnorm_nvfp4_fwd(const void *x, const void *gamma, int64_t T, int64_t
 
 mx_status mxnorm_mx_fwd(const void *x, int64_t T, int64_t d, int block, int elem, int p,
                         float coef, float eps, int scale_mode, uint8_t *codes, uint8_t *scales,
-                        float *rho, void *stream)
+                        float *rho, hipStream_t stream)
 {
     clear_error();
     const int fmt = mx_format(block, elem);
@@ -418,7 +418,7 @@ mx_status mxnorm_mx_fwd(const void *x, int64_t T, int64_t d, int block, int elem
 
 mx_status mxnorm_postround_mx_fwd(const void *x, int64_t T, int64_t d, int block, int elem,
                                   float eps, int scale_mode, uint8_t *codes, uint8_t *scales,
-                                  float *rho, void *stream)
+                                  float *rho, hipStream_t stream)
 {
     clear_error();
     const int fmt = mx_format(block, elem);
@@ -456,7 +456,7 @@ int mxnorm_postround_table(int block, float *x, float *v)
 
 mx_status rmsnorm_mx_fwd(const void *x, const void *gamma, int64_t T, int64_t d, int block,
                          int elem, float eps, int scale_mode, uint8_t *codes, uint8_t *scales,
-                         float *rho, void *stream)
+                         float *rho, hipStream_t stream)
 {
     clear_error();
     const int fmt = mx_format(block, elem);
@@ -473,7 +473,7 @@ mx_status rmsnorm_mx_fwd(const void *x, const void *gamma, int64_t T, int64_t d,
 }
 
 mx_status mx_cast_fwd(const void *x, const void *gamma, int64_t T, int64_t d, int block,
-                      int elem, int scale_mode, uint8_t *codes, uint8_t *scales, void *stream)
+                      int elem, int scale_mode, uint8_t *codes, uint8_t *scales, hipStream_t stream)
 {
     clear_error();
     const int fmt = mx_format(block, elem);

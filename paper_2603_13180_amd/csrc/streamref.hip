@@ -120,7 +120,7 @@ __global__ void __launch_bounds__(256) ste_stream_kernel(const uint4 *x, const u
 } // namespace
 
 extern "C" int mx_stream_reference_ste(const void *x, const void *grad_z, int64_t T, int64_t d,
-                                       void *out, void *stream)
+                                       void *out, hipStream_t stream)
 {
     if (T < 0 || d <= 0 || d % 512 != 0 || d > 4096 || T > ((int64_t)1 << 34))
         return 1;
@@ -136,7 +136,7 @@ extern "C" int mx_stream_reference_ste(const void *x, const void *grad_z, int64_
 }
 
 extern "C" int mx_stream_reference(const void *x, int64_t T, int64_t d, uint8_t *out,
-                                   uint8_t *out_small, int mode, void *stream)
+                                   uint8_t *out_small, int mode, hipStream_t stream)
 {
     if (T < 0 || d <= 0 || d % 512 != 0 || d > 4096 || T > ((int64_t)1 << 34))
         return 1;

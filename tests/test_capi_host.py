@@ -73,7 +73,9 @@ def test_header_compiles_as_c():
     with tempfile.TemporaryDirectory() as d:
         src = os.path.join(d, "t.c")
         open(src, "w").write('#include "mxnorm.h"\nint main(void){return MX_OK;}\n')
-        subprocess.run(["gcc", "-std=c99", "-Wall", "-Werror", "-I", os.path.dirname(HEADER),
+        # host C code that includes HIP's runtime API names the platform
+        subprocess.run(["gcc", "-std=c99", "-Wall", "-Werror", "-D__HIP_PLATFORM_AMD__",
+                        "-I", os.path.dirname(HEADER), "-I", "/opt/rocm/include",
                         "-c", src, "-o", os.path.join(d, "t.o")], check=True)
 
 

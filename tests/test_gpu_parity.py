@@ -313,6 +313,33 @@ def test_stress_preset_every_zero_and_constant_row():
     check_preset(w, dev_bf16(w.x), dev_bf16(w.gamma), xs, rows, ("rceil", "floor"), name)
 
 
+# ------------------------------------------------------ two-part contract --
+#
+# The reading of R7: a kernel's rho within 1e-6 of the oracle's double, and
+# its scale bytes and codes bit-exact against the oracle's cast of the
+# kernel's own rho.  The tests above demand more (rho bit-equal to the
+# oracle's float); this holds the cast stage to its own definition whatever
+# rho came out, so a change in the statistic's rounding could not hide a
+# cast error behind a rho mismatch, or the other way round.
+
+@pytest.mark.parametrize("B,elem", [(16, "e4m3"), (32, "e4m3"), (64, "e4m3"), (16, "e2m1"),
+                                    (32, "e2m1"), (64, "e2m1")])
+def test_cast_follows_the_kernels_own_rho(B, elem):
+    xs = [synth.generate("llama3-8b-d4096", rows=np.arange(2048)).x,
+          adversarial_rows(1024, seed=B), synth.gaussian(333, 2048, seed=B, scale=0.01)]
+    for xb in xs:
+        x = dev_bf16(xb)
+        for mode in ("rceil", "floor"):
+            codes, scales, rho = mxnorm.mxnorm_mx_fwd(x, block=B, elem=elem, scale_mode=mode)
+            c, sc, r = codes.cpu().numpy(), scales.cpu().numpy(), rho.cpu().numpy()
+            wc, ws = oracle.cast_given_rho(xb, r, B=B, elem=elem, mode=mode)
+            assert np.array_equal(sc, ws), "scales differ (B=%d %s %s)" % (B, elem, mode)
+            assert np.array_equal(c, wc), "codes differ (B=%d %s %s)" % (B, elem, mode)
+            _, _, _, r64 = oracle.mxnorm_mx(xb, B=B, elem=elem, mode=mode)
+            fin = np.isfinite(r64) & (r64 != 0) & np.isfinite(r)
+            assert (np.abs(r[fin] - r64[fin]) <= 1e-6 * np.abs(r64[fin])).all()
+
+
 # ------------------------------------------------------- buffer hygiene --
 
 def test_canaries_untouched_and_outputs_fully_written():

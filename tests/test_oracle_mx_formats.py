@@ -157,3 +157,27 @@ def test_mxfp8_b32_generic_equals_specialised():
     b = oracle.mxnorm_mxfp8(x)
     for u, v in zip(a, b):
         assert np.array_equal(u, v)
+
+
+@pytest.mark.parametrize("B", [16, 32, 64])
+@pytest.mark.parametrize("elem", ["e4m3", "e2m1"])
+@pytest.mark.parametrize("mode", ["rceil", "floor"])
+def test_cast_given_rho_is_the_cast_stage(B, elem, mode):
+    # with the oracle's own rho it reproduces Algorithm 2 exactly, non-finite
+    # and zero rows included; with any other rho it is the plain MX cast of
+    # RN32(x rho), itself pinned above and in the codec tests
+    rng = np.random.default_rng(B + len(elem) + len(mode))
+    x = bf16(rng.standard_normal((12, 512)) * np.exp(rng.uniform(-6, 6, (12, 1))))
+    x[3] = 0
+    x[4, 7] = 0x7FC0                      # NaN
+    x[5, 100] = 0xFF80                    # -Inf
+    x[6] = bf16(np.full(512, 2.5))
+    c, s, r32, _ = oracle.mxnorm_mx(x, B=B, elem=elem, mode=mode)
+    c2, s2 = oracle.cast_given_rho(x, r32, B=B, elem=elem, mode=mode)
+    assert np.array_equal(c, c2) and np.array_equal(s, s2)
+    fin = np.isfinite(synth.bf16_bits_to_f32(x)).all(1)
+    rho = np.nextafter(r32, np.float32(np.inf)) * np.float32(3.0)
+    c3, s3 = oracle.cast_given_rho(x[fin], rho[fin], B=B, elem=elem, mode=mode)
+    xf = synth.bf16_bits_to_f32(x[fin])
+    c4, s4 = oracle.mxcast((xf * rho[fin][:, None]).astype(np.float32), B=B, elem=elem, mode=mode)
+    assert np.array_equal(c3, c4) and np.array_equal(s3, s4)
