@@ -24,10 +24,11 @@
 // consecutive rows hit distinct banks.
 //
 // What bounds it: at 256 x 256 the operand stream is 64 KB per K step per
-// workgroup, about 10 TB/s of 64-byte L2 requests at half the fp8 peak, and
-// the L2 channels are busy ~94% of the kernel's time (rocprofv3 TCC_BUSY at
-// the QKV shape).  The register file holds at most about this output tile
-// (its accumulators are half of it), and LDS at most two stages of it.
+// workgroup, about 10 TB/s of 64-byte L2 requests at half the fp8 peak; with
+// the products switched off the DMA alone takes ~90% of the kernel's time,
+// and the L2 channels have requests ~94% of it (rocprofv3 TCC_BUSY at the
+// QKV shape).  The register file holds at most about this output tile (its
+// accumulators are half of it), and LDS at most two stages of it.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
