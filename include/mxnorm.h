@@ -58,6 +58,7 @@ extern "C" {
 #define MXNORM_ABI_VERSION 1
 #define MXNORM_MAX_D 32768
 #define MX_MATMUL_MAX_K (1 << 22)
+#define MX_MATMUL_MAX_N (1 << 24)
 
 typedef enum {
     MX_OK = 0,
@@ -201,7 +202,8 @@ typedef enum {
  * code gives NaN; results beyond the float range are infinite.
  * block: 32 (other sizes: MX_EUNSUPPORTED).  elem: mx_elem.  Requirements:
  * K a multiple of 128 (E4M3) or 256 (E2M1) and at most MX_MATMUL_MAX_K, N a
- * multiple of 16 (else MX_EUNSUPPORTED); codes 16-byte, scales 4-byte and out
+ * multiple of 16 and at most MX_MATMUL_MAX_N (else MX_EUNSUPPORTED); codes
+ * 16-byte, scales 4-byte and out
  * 16-byte aligned (else MX_EINVAL).  M == 0 or N == 0 is a no-op.  Asynchronous on
  * `stream`; nothing is allocated.
  */

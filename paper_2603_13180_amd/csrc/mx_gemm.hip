@@ -97,8 +97,12 @@ __device__ __forceinline__ void lds_load4(const void *gbase, uint32_t off, uint3
                  : "memory");
 }
 
-// Wait until none of this wave's vector memory loads is outstanding.
-__device__ __forceinline__ void wait_vmcnt0() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+// Wait until at most N_ of this wave's vector memory operations (loads and
+// stores, which complete in issue order) are outstanding.
+template <int N_> __device__ __forceinline__ void wait_vmcnt()
+{
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N_) : "memory");
+}
 
 // Workgroup barrier without the memory fence of __syncthreads(): the fence
 // would wait for every outstanding load, including the DMA of the next step.
@@ -349,8 +353,19 @@ __device__ __forceinline__ void step_products(v4f (&acc)[FN][FM], const LDS_AS u
     column(std::integral_constant<int, 7>{});
 }
 
+// Output stores bypass the caches' normal allocation (cache policy sc0 sc1
+// nt: system scope, non-temporal): H is written once and read by a later
+// kernel, and with the default policy the stores slow the operand stream
+// more (QKV shape, E4M3 -> bf16: 720 -> 673 us).
+constexpr int kStorePolicy = 0x13;
+
+// stores per wave and tile
+template <int OUT> constexpr int kTileStores = OUT == MX_OUT_F32 ? FM * FN : FM * FN / 2;
+
 // Store the workgroup's accumulators as H[m0 .., n0 ..] (f32 or bf16), times
-// the column gain if there is one.
+// the column gain if there is one.  Every lane runs the same stores (exactly
+// kTileStores of them when the tile lies inside H); lanes outside H are
+// masked.
 template <int OUT>
 __device__ __forceinline__ void store_tile(const Args &A, const v4f (&acc)[FN][FM], int64_t m0,
                                            int64_t n0, int wm, int wn, int g, int qd)
@@ -358,44 +373,54 @@ __device__ __forceinline__ void store_tile(const Args &A, const v4f (&acc)[FN][F
     // lane (g, qd) of tile (i, j) holds H[m][n .. n+3] with
     // m = m0 + wm + 16 j + qd and n = n0 + wn + 16 i + 4 g.  N is a multiple
     // of 16, so a tile column base below N has its 16 columns inside H.
+    // The gains of the lane's columns are loaded before any store.
+    uint2 gw[FN];
+    if (A.bgain) {
+#pragma unroll
+        for (int i = 0; i < FN; ++i) {
+            const int64_t n = n0 + wn + 16 * i + 4 * g;
+            gw[i] = *reinterpret_cast<const uint2 *>(A.bgain + (n < A.N ? n : 0));
+        }
+    }
     auto gained = [&](int i, int j) {
         v4f v = acc[i][j];
         if (A.bgain) {
-            const int64_t n = n0 + wn + 16 * i + 4 * g;
-            const uint2 gw = *reinterpret_cast<const uint2 *>(A.bgain + (n < A.N ? n : 0));
-            v[0] = v[0] * __uint_as_float(gw.x << 16);
-            v[1] = v[1] * __uint_as_float(gw.x & 0xFFFF0000u);
-            v[2] = v[2] * __uint_as_float(gw.y << 16);
-            v[3] = v[3] * __uint_as_float(gw.y & 0xFFFF0000u);
+            v[0] = v[0] * __uint_as_float(gw[i].x << 16);
+            v[1] = v[1] * __uint_as_float(gw[i].x & 0xFFFF0000u);
+            v[2] = v[2] * __uint_as_float(gw[i].y << 16);
+            v[3] = v[3] * __uint_as_float(gw[i].y & 0xFFFF0000u);
         }
         return v;
     };
-    if constexpr (OUT == MX_OUT_F32) {
+    constexpr int ES = OUT == MX_OUT_F32 ? 4 : 2; // bytes per element
 #pragma unroll
-        for (int j = 0; j < FM; ++j) {
-            const int64_t m = m0 + wm + 16 * j + qd;
+    for (int j = 0; j < FM; ++j) {
+        // buffer over the 16 rows of tile row j (byte offsets below 2^31:
+        // the host limits N)
+        const int64_t mr = m0 + wm + 16 * j;
+        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+            static_cast<uint8_t *>(A.out) + mr * A.N * ES, 0, 0x7FFFFFFF, 0x00020000);
+        const int64_t m = mr + qd;
+        const uint32_t row = (uint32_t)(qd * A.N) * ES;
+        if constexpr (OUT == MX_OUT_F32) {
 #pragma unroll
             for (int i = 0; i < FN; ++i) {
                 const int64_t n = n0 + wn + 16 * i + 4 * g;
                 const v4f v = gained(i, j);
                 if (m < A.M && n < A.N)
-                    *reinterpret_cast<float4 *>(static_cast<float *>(A.out) + m * A.N + n) =
-                        make_float4(v[0], v[1], v[2], v[3]);
+                    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), rs,
+                                                           (int)(row + (uint32_t)n * 4), 0,
+                                                           kStorePolicy);
             }
-        }
-    } else {
-        // bf16: tiles i and i+1 are stored together.  v_permlane16_swap
-        // trades the odd lane rows (g = 1, 3) of tile i's values with the
-        // even lane rows (g = 0, 2) of tile i+1's, after which lane row g
-        // holds 8 adjacent columns, 16 bytes, of tile i + (g & 1) from
-        // column 8 (g >> 1): one 16-byte store per lane and tile pair
-        // instead of two 8-byte stores.  The swap runs on every lane; only
-        // the stores are masked.
-        static_assert(FN % 2 == 0, "tiles are stored in pairs");
-        typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
-#pragma unroll
-        for (int j = 0; j < FM; ++j) {
-            const int64_t m = m0 + wm + 16 * j + qd;
+        } else {
+            // bf16: tiles i and i+1 are stored together.  v_permlane16_swap
+            // trades the odd lane rows (g = 1, 3) of tile i's values with the
+            // even lane rows (g = 0, 2) of tile i+1's, after which lane row g
+            // holds 8 adjacent columns, 16 bytes, of tile i + (g & 1) from
+            // column 8 (g >> 1): one 16-byte store per lane and tile pair
+            // instead of two 8-byte stores.  The swap runs on every lane; only
+            // the stores are masked.
+            static_assert(FN % 2 == 0, "tiles are stored in pairs");
 #pragma unroll
             for (int i = 0; i < FN; i += 2) {
                 uint32_t lo[2], hi[2];
@@ -409,8 +434,9 @@ __device__ __forceinline__ void store_tile(const Args &A, const v4f (&acc)[FN][F
                 const auto sh = __builtin_amdgcn_permlane16_swap(hi[0], hi[1], false, false);
                 const int64_t n = n0 + wn + 16 * (i + (g & 1)) + 8 * (g >> 1);
                 if (m < A.M && n < A.N)
-                    *reinterpret_cast<u32x4v *>(static_cast<uint16_t *>(A.out) + m * A.N + n) =
-                        u32x4v{sl[0], sh[0], sl[1], sh[1]};
+                    __builtin_amdgcn_raw_buffer_store_b128(u32x4{sl[0], sh[0], sl[1], sh[1]}, rs,
+                                                           (int)(row + (uint32_t)n * 2), 0,
+                                                           kStorePolicy);
             }
         }
     }
@@ -468,6 +494,7 @@ __global__ void __launch_bounds__(NT) mx_gemm_kernel(Args A)
     // last step's products and the tile's stores.
     issue_step<ELEM>(A.a + m0 * A.rb, A.b + n0 * A.rb, A.as + m0 * A.rs, A.bs + n0 * A.rs, R, 0,
                      st0_addr, w);
+    bool prev_full = false; // the previous tile lies inside H (all its stores ran)
     for (int gs = 0;;) {
         v4f acc[FN][FM];
 #pragma unroll
@@ -479,7 +506,14 @@ __global__ void __launch_bounds__(NT) mx_gemm_kernel(Args A)
         int64_t m1 = 0, n1 = 0;
         for (int s = 0; s < A.steps; ++s, ++gs) {
             const int cur = gs & 1;
-            wait_vmcnt0();
+            // this step's DMA has landed.  In a tile's first step the
+            // previous tile's stores, issued after this DMA, need not have
+            // completed: operations complete in order, so at most that many
+            // may remain (a partial tile ran fewer stores: wait for all).
+            if (s == 0 && prev_full)
+                wait_vmcnt<kTileStores<OUT>>();
+            else
+                wait_vmcnt<0>();
             barrier();
             const uint32_t nxt = st0_addr + (cur ^ 1) * STAGE;
             if (s + 1 < A.steps) {
@@ -494,6 +528,7 @@ __global__ void __launch_bounds__(NT) mx_gemm_kernel(Args A)
             step_products<ELEM>(acc, st0 + cur * STAGE, ba, bb);
         }
         store_tile<OUT>(A, acc, m0, n0, wm, wn, g, qd);
+        prev_full = m0 + BM <= A.M && n0 + BN <= A.N;
         if (nv >= G)
             break;
         v = nv;
@@ -579,8 +614,8 @@ mx_status mx_matmul_fwd(const uint8_t *a_codes, const uint8_t *a_scales, const u
         return mxk::fail(MX_EINVAL, "codes and out must be 16-byte, scales 4-byte and b_gain "
                                "8-byte aligned");
     const int64_t tm = (M + mxg::BM - 1) / mxg::BM, tn = (N + mxg::BN - 1) / mxg::BN;
-    if (tm * tn > INT32_MAX / 2 || M > INT32_MAX || N > INT32_MAX)
-        return mxk::fail(MX_EUNSUPPORTED, "problem too large");
+    if (tm * tn > INT32_MAX / 2 || M > INT32_MAX || N > MX_MATMUL_MAX_N)
+        return mxk::fail(MX_EUNSUPPORTED, "problem too large (N at most %d)", MX_MATMUL_MAX_N);
     mxg::Args A;
     A.a = a_codes;
     A.as = a_scales;
