@@ -201,6 +201,7 @@ def test_mx_cast_rejects_bad_arguments():
     (dict(bs=OUT + 2), 1), (dict(out=A8), 1), (dict(M=0, a=None, out=None), 0),
     (dict(N=0, b=None, out=None), 0), (dict(gain=OUT + 4), 1), (dict(K=1 << 23), 2),
     (dict(out=A8, out_dtype=1), 1),    # bf16 output is stored 16 bytes at a time
+    (dict(N=(1 << 24) + 16), 2),       # N beyond MX_MATMUL_MAX_N
 ])
 def test_mx_matmul_rejects_bad_arguments(args, status):
     lib = mxnorm.load()
