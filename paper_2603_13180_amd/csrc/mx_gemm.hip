@@ -325,13 +325,27 @@ __device__ __forceinline__ void step_products(v4f (&acc)[FN][FM], const LDS_AS u
         pass(std::integral_constant<int, 1>{});
         return;
     }
+    // The step starts with every wave reading fragments after the barrier:
+    // B0, B1 and A0 first, so that the first two products wait for three
+    // fragments, not six (QKV shape: 1-3% faster; the E2M1 passes above keep
+    // the plain order, which needs fewer registers).
     Frag fb[FN], fa[FM];
     fb[0] = read_frag<ELEM, 0>(st, bb);
     fb[1] = read_frag<ELEM, 1>(st, bb);
+    fa[0] = read_frag<ELEM, 0>(st, ba);
+    __builtin_amdgcn_sched_barrier(0);
     fb[2] = read_frag<ELEM, 2>(st, bb);
     fb[3] = read_frag<ELEM, 3>(st, bb);
-    fa[0] = read_frag<ELEM, 0>(st, ba);
     fa[1] = read_frag<ELEM, 1>(st, ba);
+    __builtin_amdgcn_sched_barrier(0);
+    fa[2] = read_frag<ELEM, 2>(st, ba);
+    __builtin_amdgcn_sched_barrier(0);
+    mma<ELEM>(acc[0][0], fb[0], fa[0]);
+    mma<ELEM>(acc[1][0], fb[1], fa[0]);
+    __builtin_amdgcn_sched_barrier(0);
+    mma<ELEM>(acc[2][0], fb[2], fa[0]);
+    mma<ELEM>(acc[3][0], fb[3], fa[0]);
+    __builtin_amdgcn_sched_barrier(0);
     auto column = [&](auto jc) {
         constexpr int j = decltype(jc)::value;
         if constexpr (j + 2 < FM)
@@ -343,7 +357,6 @@ __device__ __forceinline__ void step_products(v4f (&acc)[FN][FM], const LDS_AS u
             mma<ELEM>(acc[i][j], fb[i], fa[j]);
         __builtin_amdgcn_sched_barrier(0);
     };
-    column(std::integral_constant<int, 0>{});
     column(std::integral_constant<int, 1>{});
     column(std::integral_constant<int, 2>{});
     column(std::integral_constant<int, 3>{});
