@@ -24,11 +24,13 @@
 // consecutive rows hit distinct banks.
 //
 // What bounds it: at 256 x 256 the operand stream is 64 KB per K step per
-// workgroup, about 10 TB/s of 64-byte L2 requests at half the fp8 peak; with
-// the products switched off the DMA alone takes ~90% of the kernel's time,
-// and the L2 channels have requests ~94% of it (rocprofv3 TCC_BUSY at the
-// QKV shape).  The register file holds at most about this output tile (its
-// accumulators are half of it), and LDS at most two stages of it.
+// workgroup, about 10 TB/s of L2 requests at half the fp8 peak.  Two stages
+// fill LDS, so the DMA runs one step ahead of the products and each step
+// waits for it; the tile's stores slow the operand stream (the non-temporal
+// policy below halves that); and after each step's barrier every wave reads
+// fragments before its first product.  The eight waves' accumulators fill
+// half the register file, which leaves no room for a third stage in
+// registers.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
