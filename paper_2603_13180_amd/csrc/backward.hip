@@ -39,12 +39,10 @@ using namespace mxk;
 
 constexpr int CT_ROWS = 128;  // tile rows (four 32-row blocks)
 
-// Tile shapes: COLS tile columns (64 per pass of the 256 threads), at most
-// TILES tiles per workgroup.
-template <int COLS> struct CtShape {
-    static constexpr int TILES = COLS == 256 ? 8 : 16;
+// Tile shape: 128 rows x COLS columns, staged by NTH threads.
+template <int COLS, int NTH> struct CtShape {
     static constexpr int CPR = COLS / 8;          // 16-byte chunks per tile row
-    static constexpr int RPP = 256 / CPR;         // tile rows per staging pass
+    static constexpr int RPP = NTH / CPR;         // tile rows per staging pass
     static constexpr int NLD = CT_ROWS / RPP;     // staging loads per thread
     static constexpr int PITCH = COLS * 2;        // bytes per staged row
     static constexpr int BLKB = 32 * PITCH + 32;  // bytes per staged 32-row block
@@ -57,8 +55,8 @@ struct CastTArgs {
     uint8_t *codes;
     uint8_t *scales;
     int64_t R, C;
+    int64_t tile_r0; // row tile of blockIdx.y == 0 (launches of at most 65535 row tiles)
     int mode;
-    int tiles; // tiles per span, 1 .. CtShape<COLS>::TILES
 };
 
 // Lane (cc, blk) of a cast pass: column cc of the staged tile over rows
@@ -75,7 +73,7 @@ __device__ __forceinline__ uint32_t cast_block(const CastTArgs &A, const uint8_t
                                                const float *rs, int cc, int blk, int64_t orow,
                                                int64_t rb)
 {
-    using S = CtShape<COLS>;
+    using S = CtShape<COLS, 256>; // PITCH and BLKB do not depend on the thread count
     constexpr int CT_PITCH = S::PITCH, CT_BLKB = S::BLKB;
     // the block's 32 scaled values, read once from LDS and kept in
     // registers; their absmax as the integer max of the magnitude
@@ -173,16 +171,16 @@ __device__ __forceinline__ uint32_t cast_block(const CastTArgs &A, const uint8_t
 // zeros; no per-lane branch, which would serialise the loads).  The tile's
 // rho values travel with its rows (thread t < 128: row t), so that waiting
 // for them is not a wait for every store in flight.
-template <int COLS> struct TileLoad {
-    uint4 v[CtShape<COLS>::NLD];
+template <int COLS, int NTH> struct TileLoad {
+    uint4 v[CtShape<COLS, NTH>::NLD];
     float rv;
 };
 
-template <int COLS>
+template <int COLS, int NTH>
 __device__ __forceinline__ void fetch_tile(const CastTArgs &A, int64_t r0, int64_t c0, int tid,
-                                           TileLoad<COLS> &L)
+                                           TileLoad<COLS, NTH> &L)
 {
-    using S = CtShape<COLS>;
+    using S = CtShape<COLS, NTH>;
     const int ch = tid % S::CPR, rbase = tid / S::CPR;
     const uint32_t chunk_off = c0 + 8 * ch < A.C ? 16u * (uint32_t)ch : kOutside; // C % 8 == 0
     const uint32_t pitch = (uint32_t)A.C * 2u;
@@ -206,10 +204,10 @@ __device__ __forceinline__ void fetch_tile(const CastTArgs &A, int64_t r0, int64
 
 // The staged tile in LDS: as it is in x (2 COLS bytes per row), 32 bytes of
 // padding after every 32 rows; rho of row t in rs[t].
-template <int COLS>
-__device__ __forceinline__ void stage_tile(const TileLoad<COLS> &L, int tid, uint8_t *tile, float *rs)
+template <int COLS, int NTH>
+__device__ __forceinline__ void stage_tile(const TileLoad<COLS, NTH> &L, int tid, uint8_t *tile, float *rs)
 {
-    using S = CtShape<COLS>;
+    using S = CtShape<COLS, NTH>;
     const int ch = tid % S::CPR, rbase = tid / S::CPR;
 #pragma unroll
     for (int k = 0; k < S::NLD; ++k)
@@ -218,103 +216,43 @@ __device__ __forceinline__ void stage_tile(const TileLoad<COLS> &L, int tid, uin
         rs[tid] = L.rv;
 }
 
-// Wide matrices (C >= 8192): workgroup (span, tile_c) casts columns
-// [COLS tile_c, +COLS) over a span of `tiles` x 128 rows, 128 rows at a time
-// (the host sizes the span so that the grid still fills the chip), the next
-// tile's loads in flight in registers while the current one is cast.  The row
-// pieces read from x are what sets the tile width: 512-byte pieces (COLS =
-// 256) make the cast of a wide matrix (C = 28672) 9% faster than 256-byte
-// ones.  The tile is cast in COLS / 64 passes of 64 columns; in pass h wave w
-// casts columns 64h + 16w .. +15: lane 4 cc + b takes column 64h + 16w + cc
-// over rows 32b .. 32b+31 (cast_block).  The span's scale bytes per column
-// are gathered in LDS and written at the end, 64 contiguous bytes per output
-// row, rather than one scattered byte per tile.
-template <bool FP4, int COLS>
-__global__ void __launch_bounds__(256) cast_t_kernel(CastTArgs A)
+// Workgroup (tile_c, y) casts the 128 x COLS tile of x at columns COLS
+// tile_c and rows 128 (tile_r0 + y) (COLS = 256: 512-byte pieces of each x
+// row, 128-byte output pieces).  A tile is staged in LDS, then cast in passes of
+// 16 NW columns (NW waves): in pass h, lane 4 cc + b of wave w takes column
+// 16 NW h + 16 w + cc over rows 32 b .. 32 b + 31 (cast_block).  A column's
+// four scale bytes (blocks 0..3 of the tile) reach the quad's first lane
+// through DPP and go out as one dword when the tile is whole and R a
+// multiple of 128, else byte by byte.  One tile per workgroup with 512
+// threads was the fastest of the shapes measured on MI355X: at [32768, 4096]
+// 79 us against 83 (128-column tiles, 256 threads) and 89 (spans of four
+// 128-column tiles per workgroup, the next tile prefetched in registers, the
+// span's scale bytes gathered in LDS); at [32768, 28672] 626 against 632 us
+// (spans of 256-column tiles).
+template <bool FP4, int COLS, int NTH>
+__global__ void __launch_bounds__(NTH) cast_t_kernel(CastTArgs A)
 {
-    using S = CtShape<COLS>;
-    constexpr int CT_COLS = COLS, CT_TILES = S::TILES, CT_BLKB = S::BLKB;
-    __shared__ __attribute__((aligned(16))) uint8_t tile[4 * CT_BLKB];
-    __shared__ __attribute__((aligned(16))) float rs[CT_ROWS];
-    __shared__ __attribute__((aligned(16))) uint8_t sb[CT_COLS][CT_TILES * 4];
-
-    const int tid = threadIdx.x;
-    const int64_t span0 = (int64_t)blockIdx.y * CT_ROWS * A.tiles;
-    const int64_t c0 = (int64_t)blockIdx.x * CT_COLS;
-    const int ntiles = (int)min((int64_t)A.tiles, (A.R - span0 + CT_ROWS - 1) / CT_ROWS);
-    const int w = tid >> 6, lane = tid & 63;
-    const int blk = lane & 3; // 32-row block this lane casts
-
-    TileLoad<COLS> nxt;
-    fetch_tile<COLS>(A, span0, c0, tid, nxt);
-
-    for (int t = 0; t < ntiles; ++t) {
-        const int64_t r0 = span0 + (int64_t)t * CT_ROWS;
-        stage_tile<COLS>(nxt, tid, tile, rs);
-        lds_barrier();
-        if (t + 1 < ntiles)
-            fetch_tile<COLS>(A, r0 + CT_ROWS, c0, tid, nxt);
-
-        const int64_t rb = r0 + 32 * blk; // first row of this lane's block
-#pragma unroll
-        for (int h = 0; h < CT_COLS / 64; ++h) {
-            const int cc = 64 * h + 16 * w + (lane >> 2); // column in the tile
-            const int64_t orow = c0 + cc;
-            if (rb < A.R && orow < A.C)
-                sb[cc][4 * t + blk] = (uint8_t)cast_block<FP4, COLS>(A, tile, rs, cc, blk, orow, rb);
-        }
-        lds_barrier(); // the tile is overwritten next
-    }
-
-    // the span's scale bytes: column c has 4 per tile (fewer where R ends
-    // inside the span), written as four 16-byte pieces per output row when
-    // whole and aligned, else byte by byte
-    const int64_t nblk = min((int64_t)ntiles * 4, (A.R - span0) / 32);
-#pragma unroll
-    for (int pc = tid; pc < CT_COLS * 4; pc += 256) {
-        const int sc = pc >> 2, part = pc & 3;
-        const int64_t srow = c0 + sc;
-        if (srow < A.C) {
-            uint8_t *dst = A.scales + srow * (A.R / 32) + span0 / 32;
-            const int lo = 16 * part;
-            if (lo + 16 <= nblk && (((uintptr_t)(dst + lo)) & 15) == 0) {
-                *reinterpret_cast<uint4 *>(dst + lo) = *reinterpret_cast<const uint4 *>(&sb[sc][lo]);
-            } else {
-                for (int k = lo; k < lo + 16 && k < nblk; ++k)
-                    dst[k] = sb[sc][k];
-            }
-        }
-    }
-}
-
-// Other matrices: one 128 x COLS tile per workgroup, staged and cast as in
-// cast_t_kernel, with no span, no register prefetch and no scale gathering
-// (faster than spans below 8192 columns: at [32768, 4096] 83 vs 89 us, at
-// [4096, 4096] 12.4 vs 14.9 us).  A column's four scale bytes (blocks 0..3 of
-// the tile) reach the quad's first lane through DPP and go out as one dword
-// when the tile is whole and R a multiple of 128, else byte by byte.
-template <bool FP4, int COLS>
-__global__ void __launch_bounds__(256) cast_t1_kernel(CastTArgs A)
-{
-    using S = CtShape<COLS>;
+    using S = CtShape<COLS, NTH>;
+    constexpr int NW = NTH / 64;
+    static_assert(COLS % (16 * NW) == 0, "whole passes");
     __shared__ __attribute__((aligned(16))) uint8_t tile[4 * S::BLKB];
     __shared__ __attribute__((aligned(16))) float rs[CT_ROWS];
     const int tid = threadIdx.x;
-    const int64_t r0 = (int64_t)blockIdx.y * CT_ROWS;
     const int64_t c0 = (int64_t)blockIdx.x * COLS;
     const int w = tid >> 6, lane = tid & 63;
-    const int blk = lane & 3;
+    const int blk = lane & 3; // 32-row block this lane casts
+    const int64_t r0 = (A.tile_r0 + (int64_t)blockIdx.y) * CT_ROWS;
     {
-        TileLoad<COLS> L;
-        fetch_tile<COLS>(A, r0, c0, tid, L);
-        stage_tile<COLS>(L, tid, tile, rs);
+        TileLoad<COLS, NTH> L;
+        fetch_tile<COLS, NTH>(A, r0, c0, tid, L);
+        stage_tile<COLS, NTH>(L, tid, tile, rs);
     }
     lds_barrier();
-    const int64_t rb = r0 + 32 * blk;
+    const int64_t rb = r0 + 32 * blk; // first row of this lane's block
     const bool whole = r0 + CT_ROWS <= A.R && (A.R & 127) == 0;
 #pragma unroll
-    for (int h = 0; h < COLS / 64; ++h) {
-        const int cc = 64 * h + 16 * w + (lane >> 2);
+    for (int h = 0; h < COLS / (16 * NW); ++h) {
+        const int cc = 16 * NW * h + 16 * w + (lane >> 2); // column in the tile
         const int64_t orow = c0 + cc;
         uint32_t byte = 0;
         if (rb < A.R && orow < A.C)
@@ -783,33 +721,20 @@ mx_status mx_cast_t_fwd(const void *x, const float *rho, int64_t R, int64_t C, i
     A.R = R;
     A.C = C;
     A.mode = scale_mode;
-    // tile width: 256 columns from C = 8192 on, else 128 (see the kernel);
-    // tiles per workgroup: as many as keep about 2048 workgroups (longer
-    // spans write longer runs of scale bytes), at most the shape's TILES
-    const bool wide = C >= 8192;
-    const int cols = wide ? 256 : 128;
-    const int max_tiles = wide ? mxb::CtShape<256>::TILES : mxb::CtShape<128>::TILES;
-    const int64_t col_tiles = (C + cols - 1) / cols;
+    // one 128 x 256 tile per workgroup (see the kernel), at most 65535 row
+    // tiles per launch
+    constexpr int kCols = 256, kThreads = 512;
+    constexpr int64_t kMaxRowTiles = 65535;
+    const int64_t col_tiles = (C + kCols - 1) / kCols;
     const int64_t row_tiles = (R + mxb::CT_ROWS - 1) / mxb::CT_ROWS;
-    A.tiles = (int)std::max<int64_t>(1, std::min<int64_t>(max_tiles, col_tiles * row_tiles / 2048));
-    const int64_t span = (int64_t)mxb::CT_ROWS * A.tiles;
-    const dim3 grid((unsigned)col_tiles, (unsigned)((R + span - 1) / span));
-    if (grid.y > 65535u)
-        return mxk::fail(MX_EUNSUPPORTED, "R too large for one launch");
     hipStream_t st = static_cast<hipStream_t>(stream);
-    const dim3 grid1((unsigned)col_tiles, (unsigned)row_tiles); // one tile per workgroup
-    if (!wide && grid1.y > 65535u)
-        return mxk::fail(MX_EUNSUPPORTED, "R too large for one launch");
-    if (elem == MX_ELEM_E4M3) {
-        if (wide)
-            hipLaunchKernelGGL((mxb::cast_t_kernel<false, 256>), grid, dim3(256), 0, st, A);
+    for (int64_t t0 = 0; t0 < row_tiles; t0 += kMaxRowTiles) {
+        A.tile_r0 = t0;
+        const dim3 grid((unsigned)col_tiles, (unsigned)std::min<int64_t>(row_tiles - t0, kMaxRowTiles));
+        if (elem == MX_ELEM_E4M3)
+            hipLaunchKernelGGL((mxb::cast_t_kernel<false, kCols, kThreads>), grid, dim3(kThreads), 0, st, A);
         else
-            hipLaunchKernelGGL((mxb::cast_t1_kernel<false, 128>), grid1, dim3(256), 0, st, A);
-    } else {
-        if (wide)
-            hipLaunchKernelGGL((mxb::cast_t_kernel<true, 256>), grid, dim3(256), 0, st, A);
-        else
-            hipLaunchKernelGGL((mxb::cast_t1_kernel<true, 128>), grid1, dim3(256), 0, st, A);
+            hipLaunchKernelGGL((mxb::cast_t_kernel<true, kCols, kThreads>), grid, dim3(kThreads), 0, st, A);
     }
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess)
