@@ -650,6 +650,11 @@ def main():
     ms_ste_ref = time_launches(lambda i: streamref.stream_reference_ste(xs[i], gzs[i], gxo[i]),
                                n_sets, 60, 30, stream)
     ste_ref_gbps = 3 * T * d * 2 / (ms_ste_ref * 1e-3) / 1e9
+    # the column cast's traffic and tiling with no arithmetic
+    ms_ct_ref = time_launches(lambda i: streamref.stream_reference_transpose(xs[i], rho[i], tc[i],
+                                                                             ts[i]),
+                              n_sets, 60, 30, stream)
+    ct_ref_gbps = cast_t_bytes(T, d) / (ms_ct_ref * 1e-3) / 1e9
     bwd = {"ste_bwd": {"us": round(ms_ste * 1e3, 2),
                        "GB/s": round(ste_bytes(T, d) / (ms_ste * 1e-3) / 1e9, 1)},
            "cast_t_rho_x_mxfp8": {"us": round(ms_ct * 1e3, 2),
@@ -658,6 +663,9 @@ def main():
         v["pct_of_peak"] = round(100 * v["GB/s"] / PEAK_HBM_GBPS, 2)
     bwd["ste_bwd"]["stream_reference_GBps"] = round(ste_ref_gbps, 1)
     bwd["ste_bwd"]["frac_of_stream_reference"] = round(bwd["ste_bwd"]["GB/s"] / ste_ref_gbps, 4)
+    ct = bwd["cast_t_rho_x_mxfp8"]
+    ct["stream_reference_GBps"] = round(ct_ref_gbps, 1)
+    ct["frac_of_stream_reference"] = round(ct["GB/s"] / ct_ref_gbps, 4)
     del gzs, gxo, wsp, tc, ts
 
     # the MX matmul the MXNorm output feeds (Llama-3-8B QKV projection)

@@ -50,6 +50,20 @@ int mx_stream_reference(const void *x, int64_t T, int64_t d, uint8_t *out, uint8
 int mx_stream_reference_ste(const void *x, const void *grad_z, int64_t T, int64_t d, void *out,
                             hipStream_t stream);
 
+/*
+ * mx_stream_reference_transpose moves the bytes of mx_cast_t_fwd with E4M3
+ * codes and rho given, with its tiling (one 128 x 256 tile per workgroup of
+ * 512 threads, staged in LDS, 32-byte pieces per output row and lane, one
+ * scale dword per column and tile) and no arithmetic: it reads x bf16
+ * [R, C] and rho float [R], and writes out [C, R] (the high byte of each
+ * element, transposed) and out_small [C, R/32].  R a positive multiple of
+ * 128 and C of 256, each at most 65535 tiles (R == 0: nothing to do); x and
+ * out 16-byte, rho and out_small 4-byte aligned device pointers.  Return
+ * codes as mx_stream_reference.
+ */
+int mx_stream_reference_transpose(const void *x, const float *rho, int64_t R, int64_t C,
+                                  uint8_t *out, uint8_t *out_small, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -117,7 +117,79 @@ __global__ void __launch_bounds__(256) ste_stream_kernel(const uint4 *x, const u
                 make_uint4(a[j].x ^ b[j].x, a[j].y ^ b[j].y, a[j].z ^ b[j].z, a[j].w ^ b[j].w);
 }
 
+// The column cast's traffic and access pattern (mx_cast_t_fwd): one 128-row
+// x 256-column tile of x per workgroup of 512 threads, staged in LDS (32
+// bytes of padding per 32-row block), 128 rho values per tile; lane 4 cc + b
+// of wave w takes tile column 128 h + 16 w + cc over rows 32 b .. 32 b + 31
+// and writes 32 bytes (the high bytes of its 32 values) as two 16-byte
+// stores into that column's row of out [C, R]; a column's four block bytes
+// (the first high byte of each block, xor the block's rho bits) go out as one
+// dword of out_small [C, R/32].
+constexpr int kTR = 128, kTC = 256, kTT = 512;
+constexpr int kTPitch = 2 * kTC, kTBlk = 32 * kTPitch + 32;
+
+__global__ void __launch_bounds__(kTT) transpose_stream_kernel(const uint16_t *x, const float *rho,
+                                                               int64_t R, int64_t C,
+                                                               uint8_t *out, uint8_t *out_small)
+{
+    __shared__ __attribute__((aligned(16))) uint8_t tile[4 * kTBlk];
+    __shared__ float rs[kTR];
+    const int tid = threadIdx.x;
+    const int64_t c0 = (int64_t)blockIdx.x * kTC, r0 = (int64_t)blockIdx.y * kTR;
+    constexpr int CPR = kTC / 8, RPP = kTT / CPR, NLD = kTR / RPP;
+    const int ch = tid % CPR, rb = tid / CPR;
+    uint4 v[NLD];
+#pragma unroll
+    for (int k = 0; k < NLD; ++k)
+        v[k] = load_stream(reinterpret_cast<const uint4 *>(x + (r0 + rb + RPP * k) * C + c0) + ch);
+    const float rv = tid < kTR ? rho[r0 + tid] : 0.f;
+#pragma unroll
+    for (int k = 0; k < NLD; ++k) {
+        const int r = rb + RPP * k;
+        *reinterpret_cast<uint4 *>(&tile[(r >> 5) * kTBlk + (r & 31) * kTPitch + 16 * ch]) = v[k];
+    }
+    if (tid < kTR)
+        rs[tid] = rv;
+    __syncthreads();
+    const int w = tid >> 6, lane = tid & 63, b = lane & 3;
+#pragma unroll
+    for (int h = 0; h < kTC / 128; ++h) {
+        const int cc = 128 * h + 16 * w + (lane >> 2);
+        const uint8_t *col = tile + b * kTBlk + 2 * cc + 1;
+        uint32_t q[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k)
+            q[k] = (uint32_t)col[(4 * k) * kTPitch] | ((uint32_t)col[(4 * k + 1) * kTPitch] << 8) |
+                   ((uint32_t)col[(4 * k + 2) * kTPitch] << 16) |
+                   ((uint32_t)col[(4 * k + 3) * kTPitch] << 24);
+        uint4 *dst = reinterpret_cast<uint4 *>(out + (c0 + cc) * R + r0 + 32 * b);
+        dst[0] = make_uint4(q[0], q[1], q[2], q[3]);
+        dst[1] = make_uint4(q[4], q[5], q[6], q[7]);
+        const uint32_t byte = (q[0] ^ __float_as_uint(rs[32 * b])) & 0xFFu;
+        const uint32_t b1 = (uint32_t)__builtin_amdgcn_mov_dpp((int)byte, 0x55, 0xF, 0xF, false);
+        const uint32_t b2 = (uint32_t)__builtin_amdgcn_mov_dpp((int)byte, 0xAA, 0xF, 0xF, false);
+        const uint32_t b3 = (uint32_t)__builtin_amdgcn_mov_dpp((int)byte, 0xFF, 0xF, 0xF, false);
+        if (b == 0)
+            *reinterpret_cast<uint32_t *>(out_small + (c0 + cc) * (R / 32) + r0 / 32) =
+                byte | (b1 << 8) | (b2 << 16) | (b3 << 24);
+    }
+}
+
 } // namespace
+
+extern "C" int mx_stream_reference_transpose(const void *x, const float *rho, int64_t R, int64_t C,
+                                             uint8_t *out, uint8_t *out_small, hipStream_t stream)
+{
+    if (R <= 0 || C <= 0 || R % kTR != 0 || C % kTC != 0 || R / kTR > 65535 || C / kTC > 65535)
+        return R == 0 && C > 0 && C % kTC == 0 ? 0 : 1;
+    if (!x || !rho || !out || !out_small || (uintptr_t)x % 16 || (uintptr_t)rho % 4 ||
+        (uintptr_t)out % 16 || (uintptr_t)out_small % 4)
+        return 1;
+    hipLaunchKernelGGL(transpose_stream_kernel, dim3((unsigned)(C / kTC), (unsigned)(R / kTR)),
+                       dim3(kTT), 0, (hipStream_t)stream, static_cast<const uint16_t *>(x), rho, R,
+                       C, out, out_small);
+    return hipGetLastError() == hipSuccess ? 0 : 3;
+}
 
 extern "C" int mx_stream_reference_ste(const void *x, const void *grad_z, int64_t T, int64_t d,
                                        void *out, hipStream_t stream)

@@ -24,6 +24,11 @@ def load():
         lib.mx_stream_reference_ste.restype = ctypes.c_int
         lib.mx_stream_reference_ste.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
                                                 ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]
+        lib.mx_stream_reference_transpose.restype = ctypes.c_int
+        lib.mx_stream_reference_transpose.argtypes = [ctypes.c_void_p, ctypes.c_void_p,
+                                                      ctypes.c_int64, ctypes.c_int64,
+                                                      ctypes.c_void_p, ctypes.c_void_p,
+                                                      ctypes.c_void_p]
         _lib = lib
     return _lib
 
@@ -51,3 +56,16 @@ def stream_reference_ste(x, grad_z, out):
                                         ctypes.c_void_p(torch.cuda.current_stream(x.device).cuda_stream))
     if st != 0:
         raise RuntimeError("mx_stream_reference_ste failed with status %d" % st)
+
+
+def stream_reference_transpose(x, rho, out, out_small):
+    """x bf16 [R, C] (R % 128 == 0, C % 256 == 0), rho float [R], out uint8
+    [C, R], out_small uint8 [C, R/32]: the column cast's traffic and tiling
+    with no arithmetic."""
+    R, C = x.shape
+    st = load().mx_stream_reference_transpose(
+        ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(rho.data_ptr()), R, C,
+        ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(out_small.data_ptr()),
+        ctypes.c_void_p(torch.cuda.current_stream(x.device).cuda_stream))
+    if st != 0:
+        raise RuntimeError("mx_stream_reference_transpose failed with status %d" % st)

@@ -67,6 +67,17 @@ def test_ste_stream_reference_rejects_bad_arguments():
     assert f(None, None, 0, 4096, None, None) == 0           # T = 0: no-op
 
 
+def test_transpose_stream_reference_rejects_bad_arguments():
+    from paper_2603_13180_amd import streamref
+    f = streamref.load().mx_stream_reference_transpose
+    assert f(A16, OUT, 200, 256, OUT, OUT, None) == 1        # R % 128
+    assert f(A16, OUT, 128, 320, OUT, OUT, None) == 1        # C % 256
+    assert f(A8, OUT, 128, 256, OUT, OUT, None) == 1         # x alignment
+    assert f(A16, None, 128, 256, OUT, OUT, None) == 1       # rho NULL
+    assert f(A16, OUT, -128, 256, OUT, OUT, None) == 1
+    assert f(None, None, 0, 256, None, None, None) == 0      # R = 0: no-op
+
+
 def test_header_compiles_as_c():
     import subprocess
     import tempfile

@@ -271,3 +271,24 @@ def test_mxnorm_linear_backward(elem):
     gw_ref = f64(ghb).T @ (xs64 / S) * f64(gb)[None, :]
     rel = np.linalg.norm(gw.cpu().numpy() - gw_ref) / np.linalg.norm(gw_ref)
     assert rel < (0.10 if elem == "e4m3" else 0.30), rel
+
+
+def test_transpose_stream_reference_moves_the_bytes():
+    # the column cast's stream reference (a bandwidth denominator) really
+    # reads x and rho and writes the transposed bytes it claims to
+    from paper_2603_13180_amd import streamref
+    R, C = 256, 512
+    g = torch.Generator(device=DEV)
+    g.manual_seed(3)
+    x = torch.randn(R, C, generator=g, device=DEV).to(torch.bfloat16)
+    rho = torch.rand(R, generator=g, device=DEV) + 0.5
+    out = torch.empty(C, R, dtype=torch.uint8, device=DEV)
+    small = torch.empty(C, R // 32, dtype=torch.uint8, device=DEV)
+    streamref.stream_reference_transpose(x, rho, out, small)
+    torch.cuda.synchronize()
+    xb = x.view(torch.int16).cpu().numpy().astype(np.uint16)
+    hi = (xb >> 8).astype(np.uint8)
+    assert np.array_equal(out.cpu().numpy(), hi.T)
+    rb = rho.cpu().numpy().view(np.uint32)
+    want = (hi[0::32, :].T ^ (rb[0::32] & 0xFF)[None, :]).astype(np.uint8)
+    assert np.array_equal(small.cpu().numpy(), want)
