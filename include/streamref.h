@@ -44,8 +44,9 @@ int mx_stream_reference(const void *x, int64_t T, int64_t d, uint8_t *out, uint8
 /*
  * mx_stream_reference_ste moves the bytes of mxnorm_ste_bwd with bf16
  * output: it reads x and grad_z, bf16 [T, d] each, and writes out, bf16
- * [T, d] (their bitwise xor), one row per wave with 16-byte accesses.  Same
- * size and alignment rules and return codes as mx_stream_reference.
+ * [T, d] (their bitwise xor), one row per wave with 16-byte accesses, the
+ * stores with the STE kernel's cache policy (sc0 sc1 nt).  Same size and
+ * alignment rules and return codes as mx_stream_reference.
  */
 int mx_stream_reference_ste(const void *x, const void *grad_z, int64_t T, int64_t d, void *out,
                             hipStream_t stream);

@@ -278,6 +278,11 @@ __global__ void __launch_bounds__(NTH) cast_t_kernel(CastTArgs A)
 
 // ------------------------------------------------------------ STE rows --
 
+// grad_x is written once and read by a later kernel: its stores take the
+// sc0 sc1 nt cache policy (system scope, non-temporal).  At [32768, 4096]
+// on MI355X the call ran 144.5 -> 135.5 us with it (137.0 with nt alone).
+constexpr int kGradXPolicy = 0x13;
+
 // rows per workgroup (each writes one partial row of grad_gamma): 4 .. 64,
 // as many as keep about 512 workgroups, two per compute unit (at [32768,
 // 4096] on MI355X: 152.8 us, against 155.6 with 1024 workgroups and 169.6
@@ -460,18 +465,18 @@ ste_bwd_kernel(SteArgs A)
                 __builtin_amdgcn_raw_buffer_store_b128(
                     (u32x4_t){__float_as_uint(o[0]), __float_as_uint(o[1]), __float_as_uint(o[2]),
                               __float_as_uint(o[3])},
-                    outr, (int)off, 0, 0);
+                    outr, (int)off, 0, kGradXPolicy);
                 __builtin_amdgcn_raw_buffer_store_b128(
                     (u32x4_t){__float_as_uint(o[4]), __float_as_uint(o[5]), __float_as_uint(o[6]),
                               __float_as_uint(o[7])},
-                    outr, (int)(off == kOutside ? kOutside : off + 16u), 0, 0);
+                    outr, (int)(off == kOutside ? kOutside : off + 16u), 0, kGradXPolicy);
             } else {
                 uint32_t p[4];
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
                     p[i] = f32_to_bf16(o[2 * i]) | ((uint32_t)f32_to_bf16(o[2 * i + 1]) << 16);
                 __builtin_amdgcn_raw_buffer_store_b128((u32x4_t){p[0], p[1], p[2], p[3]}, outr, (int)off,
-                                                       0, 0);
+                                                       0, kGradXPolicy);
             }
         }
     };

@@ -94,7 +94,8 @@ __global__ void __launch_bounds__(256) stream_kernel(const uint4 *x, int64_t T, 
 
 // The straight-through estimator's traffic: per row, x and grad_z read and
 // grad_x written, bf16 [T, d] each, one row per wave, 16-byte accesses, all
-// loads of a row issued before its stores.
+// loads of a row issued before its stores, which take the STE kernel's
+// cache policy (sc0 sc1 nt).
 __global__ void __launch_bounds__(256) ste_stream_kernel(const uint4 *x, const uint4 *gz, int64_t T,
                                                          int nc, uint4 *out)
 {
@@ -110,11 +111,14 @@ __global__ void __launch_bounds__(256) ste_stream_kernel(const uint4 *x, const u
         a[j] = load_stream(x + c);
         b[j] = load_stream(gz + c);
     }
+    const __amdgpu_buffer_rsrc_t orr = __builtin_amdgcn_make_buffer_rsrc(
+        out + row * nc, 0, nc * 16, 0x00020000);
 #pragma unroll
     for (int j = 0; j < 8; ++j)
         if (j < cpl)
-            out[row * nc + j * 64 + lane] =
-                make_uint4(a[j].x ^ b[j].x, a[j].y ^ b[j].y, a[j].z ^ b[j].z, a[j].w ^ b[j].w);
+            __builtin_amdgcn_raw_buffer_store_b128(
+                (u32x4_t){a[j].x ^ b[j].x, a[j].y ^ b[j].y, a[j].z ^ b[j].z, a[j].w ^ b[j].w}, orr,
+                (j * 64 + lane) * 16, 0, 0x13);
 }
 
 // The column cast's traffic and access pattern (mx_cast_t_fwd): one 128-row
