@@ -645,11 +645,13 @@ mx_status mx_matmul_fwd(const uint8_t *a_codes, const uint8_t *a_scales, const u
     A.steps = (int)(A.rb / mxg::KB);
     A.tiles_m = (int)tm;
     A.tiles_n = (int)tn;
-    // Tile order, measured at d = 4096 on MI355X: contiguous tile ranges per
-    // XCD are faster up to N = 8192 (the QKV shape: 737 vs 801 us), plain
-    // round robin from N = 16384 on (the gate+up shape, N = 28672: 1765 vs
-    // 1842 us at M = 16384, and likewise at M = 4096 .. 32768).
-    A.xcd_ranges = tn < 64 ? 1 : 0;
+    // Tile order: each XCD runs a contiguous range of tiles.  Measured at
+    // d = 4096 on MI355X against plain round robin: the QKV shape 737 vs
+    // 801 us; the gate+up shape (N = 28672) 1583 vs 1715 us at M = 16384 and
+    // 3214 vs 3446 us at M = 32768 (E2M1: 958 vs 1019 us).  (Before the
+    // output stores took their non-temporal policy, round robin was the
+    // faster order from N = 16384 on.)
+    A.xcd_ranges = 1;
     // one workgroup per compute unit (each holds 135-139 KB of LDS); with the
     // count unknown, one workgroup per tile
     const int cus = compute_units(stream);
