@@ -641,19 +641,26 @@ def main():
                       device=dev)
     tc = [torch.empty(d, T, dtype=torch.uint8, device=dev) for _ in range(n_sets)]
     ts = [torch.empty(d, T // 32, dtype=torch.uint8, device=dev) for _ in range(n_sets)]
-    ms_ste = time_launches(lambda i: mxnorm.mxnorm_ste_bwd(
-        xs[i], gzs[i], g, rho[i], grad_x=gxo[i], grad_gamma=ggo, workspace=wsp),
-        n_sets, 60, 30, stream)
-    ms_ct = time_launches(lambda i: mxnorm.mx_cast_t_fwd(xs[i], rho[i], codes=tc[i], scales=ts[i]),
-                          n_sets, 60, 30, stream)
-    # the STE's traffic with no arithmetic: x and grad_Z read, grad_X written
-    ms_ste_ref = time_launches(lambda i: streamref.stream_reference_ste(xs[i], gzs[i], gxo[i]),
-                               n_sets, 60, 30, stream)
+    # each kernel beside the stream with its traffic and no arithmetic (the
+    # STE's: x and grad_Z read, grad_X written; the column cast's: its
+    # tiling, transposed bytes), in interleaved rounds after a common warm-up
+    # so that clock and power transients hit a kernel and its stream alike;
+    # per-kernel medians
+    bkern = (("ste", lambda i: mxnorm.mxnorm_ste_bwd(
+                 xs[i], gzs[i], g, rho[i], grad_x=gxo[i], grad_gamma=ggo, workspace=wsp)),
+             ("ste_ref", lambda i: streamref.stream_reference_ste(xs[i], gzs[i], gxo[i])),
+             ("ct", lambda i: mxnorm.mx_cast_t_fwd(xs[i], rho[i], codes=tc[i], scales=ts[i])),
+             ("ct_ref", lambda i: streamref.stream_reference_transpose(xs[i], rho[i], tc[i],
+                                                                       ts[i])))
+    for _, fn in bkern:
+        time_launches(fn, n_sets, 30, 0, stream)
+    btimes = {name: [] for name, _ in bkern}
+    for _ in range(7):
+        for name, fn in bkern:
+            btimes[name].append(time_launches(fn, n_sets, 20, 3, stream))
+    ms_ste, ms_ste_ref, ms_ct, ms_ct_ref = (float(np.median(btimes[k]))
+                                            for k in ("ste", "ste_ref", "ct", "ct_ref"))
     ste_ref_gbps = 3 * T * d * 2 / (ms_ste_ref * 1e-3) / 1e9
-    # the column cast's traffic and tiling with no arithmetic
-    ms_ct_ref = time_launches(lambda i: streamref.stream_reference_transpose(xs[i], rho[i], tc[i],
-                                                                             ts[i]),
-                              n_sets, 60, 30, stream)
     ct_ref_gbps = cast_t_bytes(T, d) / (ms_ct_ref * 1e-3) / 1e9
     bwd = {"ste_bwd": {"us": round(ms_ste * 1e3, 2),
                        "GB/s": round(ste_bytes(T, d) / (ms_ste * 1e-3) / 1e9, 1)},
@@ -666,6 +673,8 @@ def main():
     ct = bwd["cast_t_rho_x_mxfp8"]
     ct["stream_reference_GBps"] = round(ct_ref_gbps, 1)
     ct["frac_of_stream_reference"] = round(ct["GB/s"] / ct_ref_gbps, 4)
+    bwd["method"] = ("median of 7 interleaved rounds of 20 launches per kernel, each kernel "
+                     "beside its stream")
     del gzs, gxo, wsp, tc, ts
 
     # the MX matmul the MXNorm output feeds (Llama-3-8B QKV projection)

@@ -58,7 +58,8 @@
  *
  *
  * Parity unpinned: the paper prints no value that fixes readings R3 (the
- * value and place of epsilon), R8 (the non-finite policy), R9 (the NVFP4
+ * value and place of epsilon in MXNorm; the RMSNorm placement is checked
+ * against torch's rms_norm), R8 (the non-finite policy), R9 (the NVFP4
  * conventions: s_g, nibble order, division order) and FLOOR mode's
  * saturation (R4).  The functions that carry them are checked against their
  * written definitions and the invariants above, not against a value from the

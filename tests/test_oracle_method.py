@@ -253,6 +253,27 @@ def test_non_finite_rows():
     assert np.all(codes[2, 32:] == 0x00)
 
 
+# ------------------------------------------------ epsilon (reading R3) --
+
+@pytest.mark.parametrize("eps", [1e-6, 1e-2])
+def test_rmsnorm_epsilon_matches_torch_rms_norm(eps):
+    # The baseline's rho against torch's own RMSNorm (a separate
+    # implementation): y = x (mean x^2 + eps)^(-1/2), so rho = y / x.  Rows
+    # of magnitude 1e-4 .. 1 put mean x^2 below, near and above eps, where
+    # eps added to the RMS, to the sum or after the inversion would differ.
+    rng = np.random.default_rng(23)
+    mags = np.array([1e-4, 3e-4, 1e-3, 3e-3, 1e-2, 0.1, 1.0])
+    x = bf16(rng.standard_normal((len(mags), 256)) * mags[:, None])
+    _, _, r32, r64 = oracle.rmsnorm_mxfp8(x, None, eps=eps)
+    xf = torch.from_numpy(synth.bf16_bits_to_f32(x).astype(np.float64))
+    # the boundary's eps is a float32 argument
+    y = torch.nn.functional.rms_norm(xf, (256,), eps=float(np.float32(eps)))
+    nz = xf != 0
+    want = (y[nz] / xf[nz]).reshape(len(mags), -1)[:, 0].numpy()
+    assert np.allclose(r64, want, rtol=1e-12, atol=0)
+    assert np.array_equal(r32, r64.astype(np.float32))
+
+
 # --------------------------------------------------------- calibration --
 
 @pytest.mark.parametrize("d", [2048, 4096])
