@@ -57,6 +57,7 @@ struct CastTArgs {
     int64_t R, C;
     int64_t tile_r0; // row tile of blockIdx.y == 0 (launches of at most 65535 row tiles)
     int mode;
+    int order;       // tile visiting order, see cast_t_kernel
 };
 
 // Lane (cc, blk) of a cast pass: column cc of the staged tile over rows
@@ -238,10 +239,31 @@ __global__ void __launch_bounds__(NTH) cast_t_kernel(CastTArgs A)
     __shared__ __attribute__((aligned(16))) uint8_t tile[4 * S::BLKB];
     __shared__ __attribute__((aligned(16))) float rs[CT_ROWS];
     const int tid = threadIdx.x;
-    const int64_t c0 = (int64_t)blockIdx.x * COLS;
+    // Tile of this workgroup.  order 0: dispatch order, the column tiles of
+    // one row band after another.  order 1 (wide matrices): workgroups are
+    // dispatched round robin over the 8 XCDs; renumbered so that each XCD
+    // runs a contiguous range of a sequence that takes groups of 64 row
+    // tiles, column tile by column tile.  The 32 workgroups an XCD runs at
+    // once then write 4 KB runs of 256 output rows, where the dispatch order
+    // wrote 128-byte pieces of thousands (MI355X, [32768, 28672]: 623 ->
+    // 544 us; [16384, 28672] 308 -> 272; [32768, 14336] 286 -> 278; at 8192
+    // columns and fewer the dispatch order is faster).
+    int64_t ct = blockIdx.x, rt = blockIdx.y;
+    if (A.order) {
+        constexpr int64_t GR = 64, NX = 8;
+        const int64_t nc = gridDim.x, nr = gridDim.y, nt = nc * nr;
+        const int64_t v = ct + rt * nc;
+        const int64_t xcd = v % NX, loc = v / NX, q = nt / NX, rem = nt % NX;
+        const int64_t p = xcd < rem ? xcd * (q + 1) + loc : rem * (q + 1) + (xcd - rem) * q + loc;
+        const int64_t g = p / (GR * nc), in = p - g * GR * nc;
+        const int64_t gsz = min(GR, nr - g * GR);
+        rt = g * GR + in % gsz;
+        ct = in / gsz;
+    }
+    const int64_t c0 = ct * COLS;
     const int w = tid >> 6, lane = tid & 63;
     const int blk = lane & 3; // 32-row block this lane casts
-    const int64_t r0 = (A.tile_r0 + (int64_t)blockIdx.y) * CT_ROWS;
+    const int64_t r0 = (A.tile_r0 + rt) * CT_ROWS;
     {
         TileLoad<COLS, NTH> L;
         fetch_tile<COLS, NTH>(A, r0, c0, tid, L);
@@ -732,6 +754,7 @@ mx_status mx_cast_t_fwd(const void *x, const float *rho, int64_t R, int64_t C, i
     constexpr int64_t kMaxRowTiles = 65535;
     const int64_t col_tiles = (C + kCols - 1) / kCols;
     const int64_t row_tiles = (R + mxb::CT_ROWS - 1) / mxb::CT_ROWS;
+    A.order = col_tiles >= 48 ? 1 : 0; // from 12288 columns on (see the kernel)
     hipStream_t st = static_cast<hipStream_t>(stream);
     for (int64_t t0 = 0; t0 < row_tiles; t0 += kMaxRowTiles) {
         A.tile_r0 = t0;

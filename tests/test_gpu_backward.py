@@ -53,9 +53,11 @@ def check_cast_t(xb, rho, elem, mode):
 
 @pytest.mark.parametrize("elem", ["e4m3", "e2m1"])
 @pytest.mark.parametrize("R,C", [(32, 8), (96, 40), (160, 200), (256, 64), (1024, 1000),
-                                 (4096, 256), (64, 8200), (288, 8448)])
+                                 (4096, 256), (64, 8200), (288, 8448), (160, 12296)])
 def test_cast_t_shapes(elem, R, C):
-    # C >= 8192 takes the 256-column tiles (8200 and 8448: a ragged last tile)
+    # ragged last column tiles (8200, 8448, 12296) and row tiles (160, 288);
+    # from 48 column tiles (12288 columns) on the workgroups visit the tiles
+    # in XCD ranges of 64-row-tile groups (12296 x 160: one partial group)
     xb = synth.gaussian(R, C, seed=R + C, scale=2.0)
     rho = np.random.default_rng(R).uniform(0.01, 8.0, R).astype(np.float32)
     for mode in ("rceil", "floor"):
@@ -77,14 +79,15 @@ def test_cast_t_edge_columns(elem):
 
 
 @pytest.mark.parametrize("elem", ["e4m3", "e2m1"])
-@pytest.mark.parametrize("R,C", [(16384, 4096), (32768, 4096), (4096, 28672), (16384, 16384)])
+@pytest.mark.parametrize("R,C", [(16384, 4096), (32768, 4096), (4096, 28672), (16384, 16384),
+                                 (8320, 12288)])
 def test_cast_t_multi_tile_spans_sampled(elem, R, C):
-    """Shapes where a workgroup walks several 128-row tiles (up to 8 of 128
-    columns; up to 4 of 256 columns at [16384, 16384]; the bench's
-    [32768, 4096] and the wide grad_H of the gate+up projection):
-    output rows of sampled columns -- the first and last of column tiles and
-    random ones -- against the oracle's cast of those columns alone (an
-    output row depends only on its column and rho)."""
+    """Large shapes: the bench's [32768, 4096], the wide grad_H of the
+    gate+up projection at 4096 tokens (112 column tiles, one partial group
+    of row tiles in the XCD-range order), [16384, 16384] (two full groups)
+    and [8320, 12288] (a full group and a partial one): output rows of sampled columns -- the first and last of column
+    tiles and random ones -- against the oracle's cast of those columns
+    alone (an output row depends only on its column and rho)."""
     rng = np.random.default_rng(R + C)
     xb = synth.gaussian(R, C, seed=C, scale=3.0)
     rho = rng.uniform(0.01, 8.0, R).astype(np.float32)
