@@ -239,48 +239,12 @@ __device__ __forceinline__ Frag read_frag(const LDS_AS uint8_t *st, const FragBa
     return f;
 }
 
-// E2M1: one half of a fragment (H = 0: chunk g, block g; H = 1: chunk 4 + g,
-// block 4 + g), the operand of one matrix-core instruction
-struct Half {
-    u32x4 v;
-    int s;
-};
-
-template <int J, int H>
-__device__ __forceinline__ Half read_half(const LDS_AS uint8_t *st, const FragBase &b)
+// acc += B-fragment x A-fragment over one E4M3 K step (B is the
+// instruction's first operand: each lane's four results are then four
+// consecutive columns of one row of H)
+__device__ __forceinline__ void mma_e4m3(v4f &acc, const Frag &b, const Frag &a)
 {
-    constexpr int SB = Op<MX_ELEM_E2M1>::SB;
-    Half f;
-    f.v = *reinterpret_cast<const LDS_AS u32x4 *>(st + (H ? b.hi : b.lo) + J * 16 * KB);
-    f.s = st[b.sc + J * 16 * SB + 4 * H];
-    return f;
-}
-
-__device__ __forceinline__ void mma_half(v4f &acc, const Half &b, const Half &a)
-{
-    const u32x4 z = {0u, 0u, 0u, 0u};
-    const v8i bv = __builtin_bit_cast(v8i, __builtin_shufflevector(b.v, z, 0, 1, 2, 3, 4, 5, 6, 7));
-    const v8i av = __builtin_bit_cast(v8i, __builtin_shufflevector(a.v, z, 0, 1, 2, 3, 4, 5, 6, 7));
-    acc = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(bv, av, acc, 4, 4, 0, b.s, 0, a.s);
-}
-
-// acc += B-fragment x A-fragment over one K step (B is the instruction's
-// first operand: each lane's four results are then four consecutive columns
-// of one row of H)
-template <int ELEM>
-__device__ __forceinline__ void mma(v4f &acc, const Frag &b, const Frag &a)
-{
-    if constexpr (ELEM == MX_ELEM_E2M1) {
-        const v8i z = {0, 0, 0, 0, 0, 0, 0, 0};
-        const v8i b0 = __builtin_shufflevector(b.v, z, 0, 1, 2, 3, 8, 8, 8, 8);
-        const v8i a0 = __builtin_shufflevector(a.v, z, 0, 1, 2, 3, 8, 8, 8, 8);
-        const v8i b1 = __builtin_shufflevector(b.v, z, 4, 5, 6, 7, 8, 8, 8, 8);
-        const v8i a1 = __builtin_shufflevector(a.v, z, 4, 5, 6, 7, 8, 8, 8, 8);
-        acc = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(b0, a0, acc, 4, 4, 0, b.s0, 0, a.s0);
-        acc = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(b1, a1, acc, 4, 4, 0, b.s1, 0, a.s1);
-    } else {
-        acc = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(b.v, a.v, acc, 0, 0, 0, b.s0, 0, a.s0);
-    }
+    acc = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(b.v, a.v, acc, 0, 0, 0, b.s0, 0, a.s0);
 }
 
 // The products of one K step from the stage at st: the step's four B
@@ -291,46 +255,63 @@ __device__ __forceinline__ void step_products(v4f (&acc)[FN][FM], const LDS_AS u
                                               const FragBase &ba, const FragBase &bb)
 {
     if constexpr (ELEM == MX_ELEM_E2M1) {
-        // two passes over the 32 tiles, first the low halves of the
-        // fragments (blocks 0-3 of the step), then the high halves: an
-        // accumulator's two instructions per step sit 32 apart instead of
-        // back to back, in the same order
-        auto pass = [&](auto hc) {
-            constexpr int H = decltype(hc)::value;
-            Half hb[FN], ha[FM];
-            hb[0] = read_half<0, H>(st, bb);
-            hb[1] = read_half<1, H>(st, bb);
-            hb[2] = read_half<2, H>(st, bb);
-            hb[3] = read_half<3, H>(st, bb);
-            ha[0] = read_half<0, H>(st, ba);
-            ha[1] = read_half<1, H>(st, ba);
-            auto column = [&](auto jc) {
-                constexpr int j = decltype(jc)::value;
-                if constexpr (j + 2 < FM)
-                    ha[j + 2] = read_half<j + 2, H>(st, ba);
-                __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-                for (int i = 0; i < FN; ++i)
-                    mma_half(acc[i][j], hb[i], ha[j]);
-                __builtin_amdgcn_sched_barrier(0);
-            };
-            column(std::integral_constant<int, 0>{});
-            column(std::integral_constant<int, 1>{});
-            column(std::integral_constant<int, 2>{});
-            column(std::integral_constant<int, 3>{});
-            column(std::integral_constant<int, 4>{});
-            column(std::integral_constant<int, 5>{});
-            column(std::integral_constant<int, 6>{});
-            column(std::integral_constant<int, 7>{});
+        // Whole fragments, read in the E4M3 order below (the lane's low and
+        // high 16-byte chunks each feed one instruction: E2M1 blocks g and
+        // 4 + g of the step).  Per column, the four tiles' products of the
+        // low halves, then those of the high halves: an accumulator's two
+        // instructions sit four apart, not back to back (where the second
+        // waits for the first's result), in the same order of additions.
+        // (Two passes over the 32 tiles, every low half and then every high
+        // half from half-fragment reads, were 1.5-3% slower at the QKV and
+        // gate+up shapes.)
+        const v8i z = {0, 0, 0, 0, 0, 0, 0, 0};
+        auto lo = [&](v4f &acc, const Frag &b, const Frag &a) {
+            const v8i b0 = __builtin_shufflevector(b.v, z, 0, 1, 2, 3, 8, 8, 8, 8);
+            const v8i a0 = __builtin_shufflevector(a.v, z, 0, 1, 2, 3, 8, 8, 8, 8);
+            acc = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(b0, a0, acc, 4, 4, 0, b.s0, 0,
+                                                                   a.s0);
         };
-        pass(std::integral_constant<int, 0>{});
-        pass(std::integral_constant<int, 1>{});
+        auto hi = [&](v4f &acc, const Frag &b, const Frag &a) {
+            const v8i b1 = __builtin_shufflevector(b.v, z, 4, 5, 6, 7, 8, 8, 8, 8);
+            const v8i a1 = __builtin_shufflevector(a.v, z, 4, 5, 6, 7, 8, 8, 8, 8);
+            acc = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(b1, a1, acc, 4, 4, 0, b.s1, 0,
+                                                                   a.s1);
+        };
+        Frag fb[FN], fa[FM];
+        fb[0] = read_frag<ELEM, 0>(st, bb);
+        fb[1] = read_frag<ELEM, 1>(st, bb);
+        fa[0] = read_frag<ELEM, 0>(st, ba);
+        __builtin_amdgcn_sched_barrier(0);
+        fb[2] = read_frag<ELEM, 2>(st, bb);
+        fb[3] = read_frag<ELEM, 3>(st, bb);
+        fa[1] = read_frag<ELEM, 1>(st, ba);
+        __builtin_amdgcn_sched_barrier(0);
+        auto column = [&](auto jc) {
+            constexpr int j = decltype(jc)::value;
+            if constexpr (j + 2 < FM)
+                fa[j + 2] = read_frag<ELEM, j + 2>(st, ba);
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int i = 0; i < FN; ++i)
+                lo(acc[i][j], fb[i], fa[j]);
+#pragma unroll
+            for (int i = 0; i < FN; ++i)
+                hi(acc[i][j], fb[i], fa[j]);
+            __builtin_amdgcn_sched_barrier(0);
+        };
+        column(std::integral_constant<int, 0>{});
+        column(std::integral_constant<int, 1>{});
+        column(std::integral_constant<int, 2>{});
+        column(std::integral_constant<int, 3>{});
+        column(std::integral_constant<int, 4>{});
+        column(std::integral_constant<int, 5>{});
+        column(std::integral_constant<int, 6>{});
+        column(std::integral_constant<int, 7>{});
         return;
     }
     // The step starts with every wave reading fragments after the barrier:
     // B0, B1 and A0 first, so that the first two products wait for three
-    // fragments, not six (QKV shape: 1-3% faster; the E2M1 passes above keep
-    // the plain order, which needs fewer registers).
+    // fragments, not six (QKV shape: 1-3% faster).
     Frag fb[FN], fa[FM];
     fb[0] = read_frag<ELEM, 0>(st, bb);
     fb[1] = read_frag<ELEM, 1>(st, bb);
@@ -342,11 +323,11 @@ __device__ __forceinline__ void step_products(v4f (&acc)[FN][FM], const LDS_AS u
     __builtin_amdgcn_sched_barrier(0);
     fa[2] = read_frag<ELEM, 2>(st, ba);
     __builtin_amdgcn_sched_barrier(0);
-    mma<ELEM>(acc[0][0], fb[0], fa[0]);
-    mma<ELEM>(acc[1][0], fb[1], fa[0]);
+    mma_e4m3(acc[0][0], fb[0], fa[0]);
+    mma_e4m3(acc[1][0], fb[1], fa[0]);
     __builtin_amdgcn_sched_barrier(0);
-    mma<ELEM>(acc[2][0], fb[2], fa[0]);
-    mma<ELEM>(acc[3][0], fb[3], fa[0]);
+    mma_e4m3(acc[2][0], fb[2], fa[0]);
+    mma_e4m3(acc[3][0], fb[3], fa[0]);
     __builtin_amdgcn_sched_barrier(0);
     auto column = [&](auto jc) {
         constexpr int j = decltype(jc)::value;
@@ -356,7 +337,7 @@ __device__ __forceinline__ void step_products(v4f (&acc)[FN][FM], const LDS_AS u
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int i = 0; i < FN; ++i)
-            mma<ELEM>(acc[i][j], fb[i], fa[j]);
+            mma_e4m3(acc[i][j], fb[i], fa[j]);
         __builtin_amdgcn_sched_barrier(0);
     };
     column(std::integral_constant<int, 1>{});
