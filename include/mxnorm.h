@@ -259,7 +259,7 @@ mx_status mxnorm_ste_bwd(const void *x, const void *grad_z, const void *gamma, c
  * mxnorm_ste_bwd without a workspace argument, for callers that cannot
  * allocate device memory (code under HIP graph capture, tight serving loops,
  * harnesses that forbid hipMalloc).  Same arguments, arithmetic, outputs and
- * errors as mxnorm_ste_bwd; the grad_gamma partial rows and slices go to a
+ * errors as mxnorm_ste_bwd; the grad_gamma partial rows go to a
  * static device array of mxnorm_ste_bwd_noalloc_max_workspace() bytes
  * (32 MiB) that each GPU holds for the life of the process.  It calls no
  * hipMalloc, hipFree or allocating library routine.  Returns MX_EUNSUPPORTED,

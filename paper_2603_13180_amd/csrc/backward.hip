@@ -662,7 +662,7 @@ bool aligned(const void *p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0;
 int64_t ste_workgroups(int64_t T) { return (T + mxb::ste_rpw(T) - 1) / mxb::ste_rpw(T); }
 
 // Device-resident workspace of mxnorm_ste_bwd_noalloc: the grad_gamma partial
-// rows and slices live here instead of in caller memory.  Each GPU the
+// rows live here instead of in caller memory.  Each GPU the
 // library runs on holds its own copy for the life of the process.  In host
 // code `scratch` only names the symbol; its device address (one per GPU) is
 // looked up once per device with hipGetSymbolAddress and kept in
@@ -859,8 +859,8 @@ mx_status mxnorm_ste_bwd_noalloc(const void *x, const void *grad_z, const void *
         if (st != MX_OK)
             return st;
     }
-    // every partial row and slice is written before it is read, so the
-    // scratch needs no clearing between calls
+    // every partial row is written before it is read, so the scratch needs
+    // no clearing between calls
     return mxnorm_ste_bwd(x, grad_z, gamma, rho, T, d, out_dtype, grad_x, grad_gamma, ws,
                           ws ? kScratchBytes : 0, stream);
 }
