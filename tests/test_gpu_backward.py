@@ -170,6 +170,13 @@ def test_ste_shapes(T, d):
     check_ste(T, d, False, torch.float32, True)
 
 
+def test_ste_bench_shape():
+    # the bench's [32768, 4096]: 64 rows per workgroup (512 workgroups), the
+    # three-set row pipeline run to its end, every element of grad_x and
+    # grad_gamma compared
+    check_ste(32768, 4096, True, torch.bfloat16, True, seed=3)
+
+
 @pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
 @pytest.mark.parametrize("gamma", [True, False])
 @pytest.mark.parametrize("want_gg", [True, False])

@@ -258,11 +258,12 @@ def test_qkv_shape_sampled_rows(elem, out_dtype):
 
 
 @pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
-def test_gate_up_shape_sampled(out_dtype):
+@pytest.mark.parametrize("elem", ELEMS)
+def test_gate_up_shape_sampled(elem, out_dtype):
     # [16384, 4096] x [28672, 4096]^T: 64 x 112 tiles; sampled rows against
     # sampled columns from 24 tile columns
-    M, N, K, elem = 16384, 28672, 4096, "e4m3"
-    rng = np.random.default_rng(41)
+    M, N, K = 16384, 28672, 4096
+    rng = np.random.default_rng(41 + len(elem))
     ac, as_ = big_operand(M, K, elem, rng)
     bc, bs = big_operand(N, K, elem, rng)
     h = mxnorm.mx_matmul_fwd(dev_u8(ac), dev_u8(as_), dev_u8(bc), dev_u8(bs), K, elem=elem,
@@ -273,7 +274,7 @@ def test_gate_up_shape_sampled(out_dtype):
     got = sub.float().cpu().numpy().astype(np.float64)
     want, mag = oracle_product(ac[rows], as_[rows], bc[cols], bs[cols], K, elem)
     assert_close(got, want, mag, out_dtype == torch.bfloat16,
-                 "gate+up %s (%d x %d sampled)" % (out_dtype, len(rows), len(cols)))
+                 "gate+up %s %s (%d x %d sampled)" % (elem, out_dtype, len(rows), len(cols)))
 
 
 @pytest.mark.parametrize("elem", ELEMS)
