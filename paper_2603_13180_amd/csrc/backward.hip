@@ -307,8 +307,9 @@ constexpr int kGradXPolicy = 0x13;
 
 // rows per workgroup (each writes one partial row of grad_gamma): 4 .. 64,
 // as many as keep about 512 workgroups, two per compute unit (at [32768,
-// 4096] on MI355X: 152.8 us, against 155.6 with 1024 workgroups and 169.6
-// with 384)
+// 4096] on MI355X, with the current row pipeline: 134-136 us for the call
+// against 145 with 768 workgroups; before it, 1024 workgroups were 2% and
+// 384 11% slower)
 inline int ste_rpw(int64_t T)
 {
     return (int)std::max<int64_t>(4, std::min<int64_t>(64, (T + 511) / 512));
