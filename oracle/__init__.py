@@ -86,6 +86,12 @@ def _load():
         "mxo_postround_finv_lut": (ctypes.c_double, [ctypes.c_double, P, P]),
         "mxo_mxnorm_postround_mx": (None, [P, I64, I64, I, I, F, I, P, P, P, P]),
         "mxo_mx_matmul": (ctypes.c_int, [P, P, P, P, I64, I64, I64, I, I, P]),
+        # host mirror of the library's forward boundary (status codes as the library's)
+        "mxref_mxnorm_mxfp8_fwd": (I, [P, I64, I64, I, F, F, I, P, P, P]),
+        "mxref_rmsnorm_mxfp8_fwd": (I, [P, P, I64, I64, F, I, P, P, P]),
+        "mxref_mxnorm_nvfp4_fwd": (I, [P, I64, I64, I, F, F, F, P, P, P]),
+        "mxref_rmsnorm_nvfp4_fwd": (I, [P, P, I64, I64, F, F, P, P, P]),
+        "mxref_cast_given_rho": (I, [P, P, I64, I64, I, P, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)

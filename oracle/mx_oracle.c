@@ -75,6 +75,7 @@
  * (no FMA contraction, no flush-to-zero; x86-64 SSE arithmetic is IEEE
  * binary32/binary64 with round-to-nearest-even).
  */
+#include <float.h>
 #include <math.h>
 #include <stdint.h>
 #include <stdlib.h>
@@ -958,4 +959,121 @@ void mxo_mxnorm_postround_mx(const uint16_t *x, int64_t T, int64_t d, int B, int
         }
         store_row_codes(rowcodes, d, elem, codes + t * (elem == MXO_ELEM_E2M1 ? d / 2 : d));
     }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Host mirror of the library's forward boundary (test infrastructure): the  */
+/* argument lists of mxnorm_mxfp8_fwd, rmsnorm_mxfp8_fwd, mxnorm_nvfp4_fwd,  */
+/* rmsnorm_nvfp4_fwd and a cast for a given rho, with host pointers and no   */
+/* stream, returning the boundary's status numbers (0 ok, 1 invalid          */
+/* argument, 2 unsupported).  The argument rules are the documented ones,    */
+/* checked in the documented order before anything is written: T >= 0;       */
+/* x, codes and scales non-NULL when T > 0; d a positive multiple of the     */
+/* block; d <= 32768 (else unsupported); eps finite and >= 0; p in {1, 2};  */
+/* coef finite, <= 0 selecting the table value; scale mode RCEIL (0) or     */
+/* FLOOR (1); the NVFP4 decode scale in [FLT_MIN, FLT_MAX / 6].  Pointer     */
+/* alignment is a device-memory rule and is not mirrored.  rho may be NULL. */
+/* ------------------------------------------------------------------------ */
+enum { MXREF_OK = 0, MXREF_EINVAL = 1, MXREF_EUNSUPPORTED = 2 };
+#define MXREF_MAX_D 32768
+
+static int mxref_common(const void *x, int64_t T, int64_t d, int B, float eps,
+                        const void *codes, const void *scales)
+{
+    if (T < 0)
+        return MXREF_EINVAL;
+    if (T > 0 && (!x || !codes || !scales))
+        return MXREF_EINVAL;
+    if (d <= 0 || d % B != 0)
+        return MXREF_EINVAL;
+    if (d > MXREF_MAX_D)
+        return MXREF_EUNSUPPORTED;
+    if (!(eps >= 0.0f) || !(eps <= FLT_MAX))
+        return MXREF_EINVAL;
+    return MXREF_OK;
+}
+
+static int mxref_p_coef(int p, float *coef, int B)
+{
+    if (p != 1 && p != 2)
+        return MXREF_EINVAL;
+    if (!(*coef == *coef) || *coef > FLT_MAX || *coef < -FLT_MAX)
+        return MXREF_EINVAL;
+    if (*coef <= 0.0f)
+        *coef = mxo_coef(B, p);
+    return MXREF_OK;
+}
+
+static int mxref_mode(int mode) { return (mode == 0 || mode == 1) ? MXREF_OK : MXREF_EINVAL; }
+
+static int mxref_global_scale(float s_g)
+{
+    return (s_g >= FLT_MIN && s_g <= FLT_MAX / 6.0f) ? MXREF_OK : MXREF_EINVAL;
+}
+
+int mxref_mxnorm_mxfp8_fwd(const void *x, int64_t T, int64_t d, int p, float coef, float eps,
+                           int scale_mode, uint8_t *codes, uint8_t *scales, float *rho)
+{
+    int st = mxref_common(x, T, d, 32, eps, codes, scales);
+    if (st == MXREF_OK)
+        st = mxref_p_coef(p, &coef, 32);
+    if (st == MXREF_OK)
+        st = mxref_mode(scale_mode);
+    if (st == MXREF_OK && T > 0)
+        mxo_mxnorm_mxfp8((const uint16_t *)x, T, d, p, coef, eps, scale_mode, codes, scales, rho,
+                         NULL);
+    return st;
+}
+
+int mxref_rmsnorm_mxfp8_fwd(const void *x, const void *gamma, int64_t T, int64_t d, float eps,
+                            int scale_mode, uint8_t *codes, uint8_t *scales, float *rho)
+{
+    int st = mxref_common(x, T, d, 32, eps, codes, scales);
+    if (st == MXREF_OK)
+        st = mxref_mode(scale_mode);
+    if (st == MXREF_OK && T > 0)
+        mxo_rmsnorm_mxfp8((const uint16_t *)x, (const uint16_t *)gamma, T, d, eps, scale_mode,
+                          codes, scales, rho, NULL);
+    return st;
+}
+
+int mxref_mxnorm_nvfp4_fwd(const void *x, int64_t T, int64_t d, int p, float coef, float eps,
+                           float global_scale, uint8_t *codes, uint8_t *scales, float *rho)
+{
+    int st = mxref_common(x, T, d, 16, eps, codes, scales);
+    if (st == MXREF_OK)
+        st = mxref_p_coef(p, &coef, 16);
+    if (st == MXREF_OK)
+        st = mxref_global_scale(global_scale);
+    if (st == MXREF_OK && T > 0)
+        mxo_mxnorm_nvfp4((const uint16_t *)x, T, d, p, coef, eps, global_scale, codes, scales,
+                         rho, NULL);
+    return st;
+}
+
+int mxref_rmsnorm_nvfp4_fwd(const void *x, const void *gamma, int64_t T, int64_t d, float eps,
+                            float global_scale, uint8_t *codes, uint8_t *scales, float *rho)
+{
+    int st = mxref_common(x, T, d, 16, eps, codes, scales);
+    if (st == MXREF_OK)
+        st = mxref_global_scale(global_scale);
+    if (st == MXREF_OK && T > 0)
+        mxo_rmsnorm_nvfp4((const uint16_t *)x, (const uint16_t *)gamma, T, d, eps, global_scale,
+                          codes, scales, rho, NULL);
+    return st;
+}
+
+/* The MXFP8 cast stage for a caller's rho [T] (mxo_cast_given_rho). */
+int mxref_cast_given_rho(const void *x, const float *rho, int64_t T, int64_t d, int scale_mode,
+                         uint8_t *codes, uint8_t *scales)
+{
+    int st = mxref_common(x, T, d, 32, 0.0f, codes, scales);
+    if (st == MXREF_OK && T > 0 && !rho)
+        st = MXREF_EINVAL;
+    if (st == MXREF_OK)
+        st = mxref_mode(scale_mode);
+    if (st == MXREF_OK && T > 0)
+        mxo_cast_given_rho((const uint16_t *)x, rho, T, d, 32, MXO_ELEM_E4M3, scale_mode, codes,
+                           scales);
+    return st;
 }
